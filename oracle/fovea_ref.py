@@ -1,0 +1,273 @@
+"""Plain fp64 reference of FOVEA's per-draft-step retrieval and fusion.
+
+TEST INFRASTRUCTURE: imported only by tests, the smoke check and the benchmark's
+CPU-baseline leg.  It shares no code with the HIP library.
+
+Sources (paper section / equation):
+  * Method, "Image-specific visual memory": k_i = W_K LN(v_i), u_i = W_U LN(v_i),
+    with a validity mask m_i.
+  * Method, "State-conditioned top-K retrieval": q_n = W_Q(LN(h_n) + E_dep[l_n]),
+    s_{n,i} = q_n . k_i / sqrt(d_k); global softmax over valid keys; descending rank
+    pi_n; cardinality equation K_r (raw cardinality = smallest prefix whose normalised
+    mass reaches rho, clamped by K_min, K_max and |V|); renormalised readout over
+    the selected set.
+  * Method, "Cache-friendly hidden-vector correction" and the appendix paragraph
+    "Visual correction module": c_n = f([h_n; r_n]), g_n = sigmoid(g([h_n; r_n])), both
+    nets two biased linear layers with a 512-wide SiLU hidden layer; the scalar gate is
+    broadcast over the hidden size; h_hat = RMSNorm(h_n + g_n c_n) (Eq. hidden_correction).
+  * Algorithm 1 orders the per-node steps the same way.
+
+Readings where the paper is silent (each one is listed with its reason in the design notes):
+  * ties in the descending rank are broken by ascending memory index;
+  * if the prefix mass never reaches rho, the raw cardinality is |V| (so rho = 1 means
+    dense retrieval);
+  * d_k is the key width actually used (d_m);
+  * |V| = 0 gives K = 0 and a zero readout; the correction is still applied;
+  * LayerNorm is affine with biased variance; RMSNorm has a weight (optional: None
+    returns h + g c unnormalised, the reading used for the "gate = 0 returns h" check);
+  * the concatenation is [h; r] with h first; W_Q, W_K, W_U have no bias.
+
+Parity pins (tests/test_oracle.py): brute-force subset enumeration, closed forms for
+uniform and geometric score profiles, the dense special case against PyTorch's
+scaled-dot-product attention, LayerNorm/RMSNorm/linear against torch.nn.functional,
+the peaked case (K = 1, readout equals the value row exactly), gate = 0 and gate = 1
+special cases, invariants (mass, clamps, permutation equivariance, masking).  The
+correction MLPs at random weights have no independent numeric fixture in the paper:
+they are pinned through the gate special cases and the torch cross-check of each
+linear layer, not through a printed example.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "bf16_round",
+    "fold_gain",
+    "layer_norm",
+    "rms_norm",
+    "sigmoid",
+    "silu",
+    "projected_layer_norm",
+    "build_memory",
+    "query",
+    "scores",
+    "select_cumulative_mass",
+    "readout",
+    "correction",
+    "fuse",
+    "retrieve_fuse",
+]
+
+
+# --------------------------------------------------------------------------------------
+# elementary pieces
+# --------------------------------------------------------------------------------------
+
+
+def bf16_round(x) -> np.ndarray:
+    """Round to the nearest bfloat16 value, ties to even.
+
+    Only defined here for inputs that are exactly representable in float32 (e.g. the
+    product of two bf16 numbers), so that there is a single rounding step.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    f = x.astype(np.float32)
+    if not np.array_equal(f.astype(np.float64), x, equal_nan=True):
+        raise ValueError("bf16_round expects float32-representable inputs")
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    u = ((u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def fold_gain(W, gain, rounding: str | None):
+    """W diag(gain): a LayerNorm gain folded into the projection that follows it.
+
+    For bf16 storage the library keeps the folded weight in bf16, one rounding per
+    element of an exactly computed product; ``rounding="bf16"`` applies that same
+    rounding so both sides contract the same weight.  With a unit gain it is exact.
+    """
+    Wg = np.asarray(W, np.float64) * np.asarray(gain, np.float64)[None, :]
+    if rounding is None:
+        return Wg
+    if rounding == "bf16":
+        return bf16_round(Wg)
+    raise ValueError(f"unknown rounding {rounding!r}")
+
+
+def layer_norm(x, gain, bias, eps):
+    """LayerNorm over the last axis: biased variance, affine gain and bias."""
+    x = np.asarray(x, np.float64)
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps) * gain + bias
+
+
+def rms_norm(x, weight, eps):
+    """RMSNorm over the last axis with a weight."""
+    x = np.asarray(x, np.float64)
+    return x / np.sqrt((x * x).mean(axis=-1, keepdims=True) + eps) * weight
+
+
+def sigmoid(x):
+    x = np.asarray(x, np.float64)
+    out = np.empty_like(x)
+    pos = x >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-x[pos]))
+    ex = np.exp(x[~pos])
+    out[~pos] = ex / (1.0 + ex)
+    return out
+
+
+def silu(x):
+    x = np.asarray(x, np.float64)
+    return x * sigmoid(x)
+
+
+def projected_layer_norm(x, gain, bias, W, eps, gain_rounding=None):
+    """W LN(x) for each row of x.
+
+    With ``gain_rounding=None`` this is literally ``LN(x) @ W.T``.  With "bf16" the
+    LayerNorm gain is folded into W and rounded once (``fold_gain``); the bias term
+    stays exact: W LN(x) = (W diag(g)) xhat + W b, where xhat = (x - mu)/sqrt(var + eps).
+    """
+    x = np.asarray(x, np.float64)
+    W = np.asarray(W, np.float64)
+    if gain_rounding is None:
+        return layer_norm(x, gain, bias, eps) @ W.T
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    xhat = (x - mu) / np.sqrt(var + eps)
+    return xhat @ fold_gain(W, gain, gain_rounding).T + (W @ np.asarray(bias, np.float64))[None, :]
+
+
+# --------------------------------------------------------------------------------------
+# the method
+# --------------------------------------------------------------------------------------
+
+
+def build_memory(V, ln_g, ln_b, W_K, W_U, eps, gain_rounding=None):
+    """Per-image visual memory (Method, image-specific visual memory): keys and values
+    are the LayerNormed visual tokens projected by W_K and W_U (no bias)."""
+    keys = projected_layer_norm(V, ln_g, ln_b, W_K, eps, gain_rounding)
+    values = projected_layer_norm(V, ln_g, ln_b, W_U, eps, gain_rounding)
+    return keys, values
+
+
+def query(h, depth, ln_g, ln_b, E_dep, W_Q, eps, gain_rounding=None):
+    """State-conditioned query q_n = W_Q (LN(h_n) + E_dep[l_n]) (Method, retrieval)."""
+    depth = np.asarray(depth, np.int64)
+    E = np.asarray(E_dep, np.float64)[depth]
+    W_Q = np.asarray(W_Q, np.float64)
+    return projected_layer_norm(h, ln_g, ln_b, W_Q, eps, gain_rounding) + E @ W_Q.T
+
+
+def scores(q, keys):
+    """s_{n,i} = q_n . k_i / sqrt(d_k), with d_k the key width (Method, retrieval)."""
+    keys = np.asarray(keys, np.float64)
+    return np.asarray(q, np.float64) @ keys.T / np.sqrt(keys.shape[1])
+
+
+def select_cumulative_mass(s, valid, tau, k_min, k_max):
+    """Cumulative-mass cardinality rule for one node (Method, cardinality equation K_r).
+
+    s: scores over the request's memory (local indices); valid: boolean mask.
+    Returns a dict with K, the selected local indices in rank order, the selected mass
+    C_K, K_raw, and the full descending order and prefix masses for diagnostics.
+    """
+    s = np.asarray(s, np.float64)
+    valid = np.ones(s.shape, bool) if valid is None else np.asarray(valid, bool)
+    V = np.flatnonzero(valid)  # ascending local index
+    nV = V.size
+    if nV == 0:
+        return dict(K=0, K_raw=0, idx=np.zeros(0, np.int64), mass=0.0, n_valid=0,
+                    order=np.zeros(0, np.int64), prefix=np.zeros(0), alpha_tilde=np.zeros(0))
+    sv = s[V]
+    # global softmax over the valid keys
+    e = np.exp(sv - sv.max())
+    alpha_tilde = e / e.sum()
+    # descending rank; a stable sort of -s keeps ascending index among equal scores
+    rank = np.argsort(-sv, kind="stable")
+    order = V[rank]
+    prefix = np.cumsum(alpha_tilde[rank])
+    reached = np.flatnonzero(prefix >= tau)
+    K_raw = int(reached[0]) + 1 if reached.size else nV
+    K = min(nV, int(k_max), max(int(k_min), K_raw))
+    return dict(K=K, K_raw=K_raw, idx=order[:K].copy(), mass=float(prefix[K - 1]) if K else 0.0,
+                n_valid=nV, order=order, prefix=prefix, alpha_tilde=alpha_tilde)
+
+
+def readout(s, idx, values):
+    """Renormalised readout over the selected set (Method, readout equation):
+    alpha_i = exp(s_i) / sum_{j in I} exp(s_j); r = sum_i alpha_i u_i."""
+    values = np.asarray(values, np.float64)
+    idx = np.asarray(idx, np.int64)
+    if idx.size == 0:
+        return np.zeros(values.shape[1]), np.zeros(0)
+    sI = np.asarray(s, np.float64)[idx]
+    e = np.exp(sI - sI.max())
+    alpha = e / e.sum()
+    return alpha @ values[idx], alpha
+
+
+def correction(h, r, W_c1, b_c1, W_c2, b_c2, W_g1, b_g1, w_g2, b_g2):
+    """c = f([h; r]) and g = sigmoid(g_net([h; r])) (Method, correction; appendix,
+    visual correction module): each net is Linear -> SiLU -> Linear, biased."""
+    y = np.concatenate([np.atleast_2d(h), np.atleast_2d(r)], axis=-1)
+    a_c = silu(y @ np.asarray(W_c1, np.float64).T + b_c1)
+    c = a_c @ np.asarray(W_c2, np.float64).T + b_c2
+    a_g = silu(y @ np.asarray(W_g1, np.float64).T + b_g1)
+    g = sigmoid(a_g @ np.asarray(w_g2, np.float64) + b_g2)
+    return c, g
+
+
+def fuse(h, g, c, rms_w, eps):
+    """h_hat = RMSNorm(h + g c) (Eq. hidden_correction); rms_w=None returns h + g c."""
+    hp = np.atleast_2d(h) + np.asarray(g, np.float64)[:, None] * c
+    return hp if rms_w is None else rms_norm(hp, rms_w, eps)
+
+
+def retrieve_fuse(W, mem_off, keys, values, valid, node_off, h, depth, tau, k_min, k_max,
+                  gain_rounding=None):
+    """One draft step over a ragged batch of requests (Algorithm 1's inner loop).
+
+    W: dict of weights (q_ln_g, q_ln_b, E_dep, W_Q, W_c1, b_c1, W_c2, b_c2, W_g1, b_g1,
+    w_g2, b_g2, rms_w or None, ln_eps, rms_eps).  Request b owns memory rows
+    mem_off[b]:mem_off[b+1] and nodes node_off[b]:node_off[b+1].
+    Returns h_out, K, idx (local indices in rank order, -1 padded to k_max), gate,
+    mass (C_K), r, q, and per-node selection records.
+    """
+    h = np.asarray(h, np.float64)
+    n, d = h.shape
+    keys = np.asarray(keys, np.float64)
+    values = np.asarray(values, np.float64)
+    d_m = keys.shape[1]
+    B = len(node_off) - 1
+    q = query(h, depth, W["q_ln_g"], W["q_ln_b"], W["E_dep"], W["W_Q"], W["ln_eps"], gain_rounding)
+    K = np.zeros(n, np.int64)
+    idx = np.full((n, k_max), -1, np.int64)
+    mass = np.zeros(n)
+    r = np.zeros((n, d_m))
+    records = [None] * n
+    for b in range(B):
+        m0, m1 = int(mem_off[b]), int(mem_off[b + 1])
+        kb, ub = keys[m0:m1], values[m0:m1]
+        vb = None if valid is None else np.asarray(valid[m0:m1], bool)
+        t0, t1 = int(node_off[b]), int(node_off[b + 1])
+        if t1 == t0:
+            continue
+        sb = scores(q[t0:t1], kb) if m1 > m0 else np.zeros((t1 - t0, 0))
+        for j in range(t1 - t0):
+            sel = select_cumulative_mass(sb[j], vb, float(tau[b]), k_min, k_max)
+            nid = t0 + j
+            K[nid] = sel["K"]
+            idx[nid, : sel["K"]] = sel["idx"]
+            mass[nid] = sel["mass"]
+            r[nid], _ = readout(sb[j], sel["idx"], ub)
+            sel["s"] = sb[j]
+            records[nid] = sel
+    c, g = correction(h, r, W["W_c1"], W["b_c1"], W["W_c2"], W["b_c2"], W["W_g1"], W["b_g1"],
+                      W["w_g2"], W["b_g2"])
+    h_out = fuse(h, g, c, W.get("rms_w"), W["rms_eps"])
+    return dict(h_out=h_out, K=K, idx=idx, gate=g, mass=mass, r=r, q=q, records=records)

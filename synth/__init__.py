@@ -1,0 +1,6 @@
+"""Seeded synthetic inputs shared by the oracle side (tests, CPU baseline) and the
+library side (tests, benchmark).  Holds no arithmetic of the method itself: it only
+draws random arrays with the shapes and statistics of the paper's workloads and rounds
+them once to the storage dtype."""
+
+from .workloads import WORKLOADS, Case, Workload, make_case, make_memory_case, make_weights  # noqa: F401
