@@ -1,0 +1,117 @@
+// Device helpers shared by the kernels of the FOVEA retrieval + fusion library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fovea {
+
+typedef uint16_t bf16_t;  // bf16 kept as raw bits in memory
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;  // one 16-byte chunk
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------------
+// scalar conversions
+// ---------------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest, ties to even; NaN stays a quiet NaN, overflow rounds to inf.
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Storage element traits: T is float (fp32 storage) or bf16_t (bf16 storage).
+template <typename T>
+struct Elem;
+
+template <>
+struct Elem<float> {
+  static constexpr int kPer16B = 4;
+  __device__ __forceinline__ static float to_f32(float v) { return v; }
+  __device__ __forceinline__ static float from_f32(float v) { return v; }
+};
+
+template <>
+struct Elem<bf16_t> {
+  static constexpr int kPer16B = 8;
+  __device__ __forceinline__ static float to_f32(bf16_t v) { return bf16_bits_to_f32(v); }
+  __device__ __forceinline__ static bf16_t from_f32(float v) { return f32_to_bf16_bits(v); }
+};
+
+template <typename T>
+__device__ __forceinline__ float ld_f32(const T* p, int64_t i) {
+  return Elem<T>::to_f32(p[i]);
+}
+
+template <typename T>
+__device__ __forceinline__ void st_f32(T* p, int64_t i, float v) {
+  p[i] = Elem<T>::from_f32(v);
+}
+
+// ---------------------------------------------------------------------------------
+// wave / block reductions (wave64)
+// ---------------------------------------------------------------------------------
+
+template <typename V>
+__device__ __forceinline__ V wave_sum(V v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+// Sum over the 16 lanes that share lane / 16 (one MFMA 16x16 output row group).
+__device__ __forceinline__ float sum16(float v) {
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// ---------------------------------------------------------------------------------
+// MFMA wrappers (CDNA4 16x16 tiles, fp32 accumulate)
+//   bf16, K = 32: lane l holds A[l % 16][8 (l / 16) + 0..7] and B[8 (l / 16) + 0..7][l % 16]
+//   fp32, K = 4 : lane l holds A[l % 16][l / 16]            and B[l / 16][l % 16]
+//   output      : lane l holds D[4 (l / 16) + 0..3][l % 16]
+// ---------------------------------------------------------------------------------
+
+__device__ __forceinline__ f32x4 mfma_bf16_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Bit pattern of a float as an unsigned key whose integer order is the float order
+// (-0 is mapped onto +0 first so that the two zeros tie, as they compare equal).
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float key_to_float(uint32_t k) {
+  uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return __uint_as_float(u);
+}
+
+// Sticky data-error bits (same values as the public header).
+constexpr uint32_t kErrNodeOff = 0x1u;
+constexpr uint32_t kErrMemOff = 0x2u;
+constexpr uint32_t kErrDepth = 0x4u;
+constexpr uint32_t kErrTau = 0x8u;
+
+}  // namespace fovea

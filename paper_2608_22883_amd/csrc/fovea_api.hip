@@ -1,0 +1,453 @@
+// Host side of the C ABI declared in include/fovea.h: argument validation, the
+// context with its packed weights, the workspace layout and the launch sequence.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "fovea.h"
+#include "correct_kernels.hpp"
+#include "retrieve_kernels.hpp"
+
+using namespace fovea;
+
+struct fovea_ctx {
+  fovea_dims dims;
+  int device;
+  bool bf16;
+  size_t es;  // bytes per stored element
+  void* block;  // one allocation holding every packed array below
+  void* W_Q;    // [d_m, d] W_Q diag(q_ln_g), storage dtype
+  float* q_c1;  // [d_m] row sums of the folded W_Q
+  float* q_c2;  // [n_depth, d_m] W_Q (q_ln_b + E_dep[l])
+  void* W_KU;   // [2 d_m, d_v] [W_K ; W_U] diag(mem_ln_g)
+  float* m_c1;  // [2 d_m]
+  float* m_c2;  // [2 d_m] [W_K ; W_U] mem_ln_b
+  void* W1;     // [2 d_c, d + d_m] [W_c1 ; W_g1]
+  float* b1;    // [2 d_c]
+  void* W_c2;   // [d, d_c]
+  float* b_c2;  // [d]
+  float* w_g2;  // [d_c]
+  float b_g2;
+  float* rms_w;  // [d] or null
+  uint32_t* err;  // sticky device-data error bits
+  float2* build_stats;
+  int64_t build_stats_rows;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  if (a == nullptr || b == nullptr || na == 0 || nb == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+// Byte offsets of the retrieve_fuse workspace regions.
+struct WsLayout {
+  size_t node_req, stats, q, S, rT, a_c, gate_part, rms_part, total;
+};
+
+WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
+  const size_t es = dm.dtype == FOVEA_BF16 ? 2 : 4;
+  WsLayout L;
+  size_t o = 0;
+  L.node_req = o; o = align_up(o + n * 4);
+  L.stats = o; o = align_up(o + n * 8);
+  L.q = o; o = align_up(o + n * dm.d_m * (dm.dtype == FOVEA_BF16 ? 2 * kQSplitBf16 : 4));
+  L.S = o; o = align_up(o + n * m_max * 4);
+  L.rT = o; o = align_up(o + n * dm.d_m * es);
+  L.a_c = o; o = align_up(o + n * dm.d_c * es);
+  L.gate_part = o; o = align_up(o + n * (dm.d_c / kPartCols) * 4);
+  L.rms_part = o; o = align_up(o + n * (dm.d / kPartCols) * 4);
+  L.total = o;
+  return L;
+}
+
+bool dims_ok(const fovea_dims* d) {
+  if (d == nullptr) return false;
+  if (d->dtype != FOVEA_F32 && d->dtype != FOVEA_BF16) return false;
+  if (d->d <= 0 || d->d_v <= 0 || d->d_m <= 0 || d->d_c <= 0 || d->n_depth <= 0) return false;
+  if (!(d->ln_eps >= 0.f) || !(d->rms_eps >= 0.f) || !std::isfinite(d->ln_eps) ||
+      !std::isfinite(d->rms_eps))
+    return false;
+  return true;
+}
+
+bool dims_supported(const fovea_dims* d) {
+  return d->d % 64 == 0 && d->d_v % 64 == 0 && d->d_m % 64 == 0 && d->d_c % 64 == 0 &&
+         d->d <= (1 << 20) && d->d_v <= (1 << 20) && d->d_m <= (1 << 16) && d->d_c <= (1 << 16);
+}
+
+#define FOVEA_HIP(call)                                   \
+  do {                                                    \
+    if ((call) != hipSuccess) return FOVEA_ERR_DEVICE;    \
+  } while (0)
+
+template <typename T>
+fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
+  const fovea_dims& D = c->dims;
+  const int d = D.d, d_v = D.d_v, d_m = D.d_m, d_c = D.d_c;
+  auto T_ = [](const void* x) { return static_cast<const T*>(x); };
+  // folded projections
+  hipLaunchKernelGGL(fold_gain_kernel<T>, dim3(1024), dim3(256), 0, s, T_(p->W_Q), T_(p->q_ln_g),
+                     static_cast<int64_t>(d_m), d, static_cast<T*>(c->W_Q));
+  hipLaunchKernelGGL(fold_gain_kernel<T>, dim3(1024), dim3(256), 0, s, T_(p->W_K), T_(p->mem_ln_g),
+                     static_cast<int64_t>(d_m), d_v, static_cast<T*>(c->W_KU));
+  hipLaunchKernelGGL(fold_gain_kernel<T>, dim3(1024), dim3(256), 0, s, T_(p->W_U), T_(p->mem_ln_g),
+                     static_cast<int64_t>(d_m), d_v, static_cast<T*>(c->W_KU) + static_cast<int64_t>(d_m) * d_v);
+  // row sums of the folded weights and the bias / depth terms
+  auto rows = [](int items) { return dim3((items + 3) / 4); };
+  hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m), dim3(256), 0, s, static_cast<const T*>(c->W_Q),
+                     d_m, d, static_cast<const T*>(nullptr), static_cast<const T*>(nullptr), 1, c->q_c1);
+  hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m * D.n_depth), dim3(256), 0, s, T_(p->W_Q), d_m, d,
+                     T_(p->q_ln_b), T_(p->E_dep), D.n_depth, c->q_c2);
+  hipLaunchKernelGGL(row_dot_kernel<T>, rows(2 * d_m), dim3(256), 0, s, static_cast<const T*>(c->W_KU),
+                     2 * d_m, d_v, static_cast<const T*>(nullptr), static_cast<const T*>(nullptr), 1, c->m_c1);
+  hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m), dim3(256), 0, s, T_(p->W_K), d_m, d_v,
+                     T_(p->mem_ln_b), static_cast<const T*>(nullptr), 1, c->m_c2);
+  hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m), dim3(256), 0, s, T_(p->W_U), d_m, d_v,
+                     T_(p->mem_ln_b), static_cast<const T*>(nullptr), 1, c->m_c2 + d_m);
+  // correction / gate nets
+  const size_t es = sizeof(T);
+  const size_t w1_half = static_cast<size_t>(d_c) * (d + d_m) * es;
+  FOVEA_HIP(hipMemcpyAsync(c->W1, p->W_c1, w1_half, hipMemcpyDeviceToDevice, s));
+  FOVEA_HIP(hipMemcpyAsync(static_cast<char*>(c->W1) + w1_half, p->W_g1, w1_half,
+                           hipMemcpyDeviceToDevice, s));
+  FOVEA_HIP(hipMemcpyAsync(c->W_c2, p->W_c2, static_cast<size_t>(d) * d_c * es,
+                           hipMemcpyDeviceToDevice, s));
+  hipLaunchKernelGGL(to_f32_kernel<T>, dim3(8), dim3(256), 0, s, T_(p->b_c1), d_c, c->b1);
+  hipLaunchKernelGGL(to_f32_kernel<T>, dim3(8), dim3(256), 0, s, T_(p->b_g1), d_c, c->b1 + d_c);
+  hipLaunchKernelGGL(to_f32_kernel<T>, dim3(64), dim3(256), 0, s, T_(p->b_c2), d, c->b_c2);
+  hipLaunchKernelGGL(to_f32_kernel<T>, dim3(8), dim3(256), 0, s, T_(p->w_g2), d_c, c->w_g2);
+  if (c->rms_w)
+    hipLaunchKernelGGL(to_f32_kernel<T>, dim3(64), dim3(256), 0, s, T_(p->rms_w), d, c->rms_w);
+  FOVEA_HIP(hipGetLastError());
+  return FOVEA_OK;
+}
+
+template <typename T>
+fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* values, hipStream_t s) {
+  const fovea_dims& D = c->dims;
+  hipLaunchKernelGGL(row_stats_kernel<T>, dim3((n + 3) / 4), dim3(256), 0, s, n,
+                     static_cast<const T*>(V), D.d_v, D.ln_eps, c->build_stats,
+                     static_cast<const int32_t*>(nullptr), 0, static_cast<const int32_t*>(nullptr),
+                     0, 0, static_cast<const float*>(nullptr), static_cast<int32_t*>(nullptr),
+                     c->err);
+  using C = GemmCfg<T, kCorrWM, kCorrWN, kCorrTM, kCorrTN>;
+  const dim3 grid((n + C::BM - 1) / C::BM, (2 * D.d_m + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL(mem_proj_kernel<T>, grid, dim3(C::NT), 0, s, n, static_cast<const T*>(V),
+                     D.d_v, static_cast<const T*>(c->W_KU), D.d_m, c->build_stats, c->m_c1,
+                     c->m_c2, static_cast<T*>(keys), static_cast<T*>(values));
+  FOVEA_HIP(hipGetLastError());
+  return FOVEA_OK;
+}
+
+struct RFArgs {
+  int B;
+  const int64_t* mem_off;
+  int64_t n_mem;
+  int m_max;
+  const void* keys;
+  const void* values;
+  const uint8_t* valid;
+  const int32_t* node_off;
+  int n;
+  int t_max;
+  const void* h;
+  const int32_t* depth;
+  const float* tau;
+  int k_min, k_max;
+  void* h_out;
+  int32_t* k_out;
+  int32_t* idx_out;
+  float* gate_out;
+  float* mass_out;
+  float* r_out;
+  char* ws;
+};
+
+template <typename T>
+fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
+  const fovea_dims& D = c->dims;
+  const WsLayout L = ws_layout(D, a.n, a.m_max);
+  int32_t* node_req = reinterpret_cast<int32_t*>(a.ws + L.node_req);
+  float2* stats = reinterpret_cast<float2*>(a.ws + L.stats);
+  T* q = reinterpret_cast<T*>(a.ws + L.q);
+  float* S = reinterpret_cast<float*>(a.ws + L.S);
+  T* rT = reinterpret_cast<T*>(a.ws + L.rT);
+  T* a_c = reinterpret_cast<T*>(a.ws + L.a_c);
+  float* gate_part = reinterpret_cast<float*>(a.ws + L.gate_part);
+  float* rms_part = reinterpret_cast<float*>(a.ws + L.rms_part);
+  const T* h = static_cast<const T*>(a.h);
+  using C = GemmCfg<T, kCorrWM, kCorrWN, kCorrTM, kCorrTN>;
+  const int row_blocks = (a.n + C::BM - 1) / C::BM;
+
+  // 1. LayerNorm statistics of h, node -> request map, depth / tau / offset checks
+  hipLaunchKernelGGL(row_stats_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, h, D.d,
+                     D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
+                     node_req, c->err);
+  // 2. q = W_Q (LN(h) + E_dep[l])
+  hipLaunchKernelGGL(q_proj_kernel<T>, dim3(row_blocks, (D.d_m + C::BN - 1) / C::BN), dim3(C::NT),
+                     0, s, a.n, h, D.d, static_cast<const T*>(c->W_Q), D.d_m, stats, a.depth,
+                     node_req, D.n_depth, c->q_c1, c->q_c2, q);
+  // 3. scores for every (node, key) of each request
+  if (a.m_max > 0) {
+    const int tiles = (a.m_max + 63) / 64;
+    const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.d_m)));
+    hipLaunchKernelGGL(score_kernel<T>, dim3(a.B * tiles), dim3(256), 0, s, a.B, a.mem_off,
+                       a.n_mem, a.m_max, a.node_off, a.n, a.t_max, static_cast<const T*>(a.keys),
+                       D.d_m, static_cast<const T*>(q), scale, S);
+  }
+  // 4. selection and gather, one block per node
+  SelectArgs<T> sa;
+  sa.mem_off = a.mem_off;
+  sa.n_mem = a.n_mem;
+  sa.m_max = a.m_max;
+  sa.node_req = node_req;
+  sa.tau = a.tau;
+  sa.valid = a.valid;
+  sa.values = static_cast<const T*>(a.values);
+  sa.d_m = D.d_m;
+  sa.S = S;
+  sa.k_min = a.k_min;
+  sa.k_max = a.k_max;
+  sa.rT = rT;
+  sa.r_out = a.r_out;
+  sa.k_out = a.k_out;
+  sa.idx_out = a.idx_out;
+  sa.mass_out = a.mass_out;
+  sa.err = c->err;
+  const size_t sel_smem = static_cast<size_t>(a.m_max) * 4;
+  if (sel_smem > 0)
+    FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  static_cast<int>(sel_smem)));
+  hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
+  // 5. correction layer 1 (+ gate logit partials)
+  hipLaunchKernelGGL(corr1_kernel<T>, dim3(row_blocks, (2 * D.d_c + C::BN - 1) / C::BN),
+                     dim3(C::NT), 0, s, a.n, h, D.d, rT, D.d_m, static_cast<const T*>(c->W1),
+                     c->b1, D.d_c, c->w_g2, a_c, gate_part);
+  // 6. correction layer 2, gate, residual (+ RMS partials)
+  T* h_out = static_cast<T*>(a.h_out);
+  hipLaunchKernelGGL(corr2_kernel<T>, dim3(row_blocks, (D.d + C::BN - 1) / C::BN), dim3(C::NT),
+                     0, s, a.n, a_c, D.d_c, static_cast<const T*>(c->W_c2), D.d, c->b_c2,
+                     gate_part, c->b_g2, h, h_out, a.gate_out, rms_part, c->rms_w ? 1 : 0);
+  // 7. RMSNorm
+  if (c->rms_w)
+    hipLaunchKernelGGL(rms_kernel<T>, dim3(a.n), dim3(256), 0, s, a.n, D.d, rms_part, c->rms_w,
+                       D.rms_eps, h_out);
+  FOVEA_HIP(hipGetLastError());
+  return FOVEA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fovea_abi_version(void) { return FOVEA_ABI_VERSION; }
+
+const char* fovea_status_str(fovea_status st) {
+  switch (st) {
+    case FOVEA_OK: return "ok";
+    case FOVEA_ERR_INVALID_ARG: return "invalid argument";
+    case FOVEA_ERR_UNSUPPORTED: return "unsupported size";
+    case FOVEA_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case FOVEA_ERR_DEVICE: return "HIP runtime error";
+    case FOVEA_ERR_DATA: return "device-side data error";
+  }
+  return "unknown status";
+}
+
+fovea_status fovea_create(fovea_ctx** out, const fovea_dims* dims, const fovea_params* p,
+                          hipStream_t stream) {
+  if (out == nullptr) return FOVEA_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!dims_ok(dims) || p == nullptr) return FOVEA_ERR_INVALID_ARG;
+  const void* required[] = {p->mem_ln_g, p->mem_ln_b, p->W_K, p->W_U, p->q_ln_g, p->q_ln_b,
+                            p->E_dep,    p->W_Q,      p->W_c1, p->b_c1, p->W_c2, p->b_c2,
+                            p->W_g1,     p->b_g1,     p->w_g2};
+  for (const void* r : required)
+    if (r == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (std::isnan(p->b_g2)) return FOVEA_ERR_INVALID_ARG;
+  if (!dims_supported(dims)) return FOVEA_ERR_UNSUPPORTED;
+
+  fovea_ctx* c = new (std::nothrow) fovea_ctx();
+  if (c == nullptr) return FOVEA_ERR_DEVICE;
+  c->dims = *dims;
+  c->bf16 = dims->dtype == FOVEA_BF16;
+  c->es = c->bf16 ? 2 : 4;
+  c->b_g2 = p->b_g2;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return FOVEA_ERR_DEVICE;
+  }
+  const int64_t d = dims->d, d_v = dims->d_v, d_m = dims->d_m, d_c = dims->d_c, nd = dims->n_depth;
+  size_t o = 0;
+  const size_t oWQ = o; o = align_up(o + d_m * d * c->es);
+  const size_t oQc1 = o; o = align_up(o + d_m * 4);
+  const size_t oQc2 = o; o = align_up(o + nd * d_m * 4);
+  const size_t oWKU = o; o = align_up(o + 2 * d_m * d_v * c->es);
+  const size_t oMc1 = o; o = align_up(o + 2 * d_m * 4);
+  const size_t oMc2 = o; o = align_up(o + 2 * d_m * 4);
+  const size_t oW1 = o; o = align_up(o + 2 * d_c * (d + d_m) * c->es);
+  const size_t oB1 = o; o = align_up(o + 2 * d_c * 4);
+  const size_t oWc2 = o; o = align_up(o + d * d_c * c->es);
+  const size_t oBc2 = o; o = align_up(o + d * 4);
+  const size_t oWg2 = o; o = align_up(o + d_c * 4);
+  const size_t oRms = o; o = align_up(o + d * 4);
+  const size_t oErr = o; o = align_up(o + 4);
+  if (hipMalloc(&c->block, o) != hipSuccess) {
+    delete c;
+    return FOVEA_ERR_DEVICE;
+  }
+  char* base = static_cast<char*>(c->block);
+  c->W_Q = base + oWQ;
+  c->q_c1 = reinterpret_cast<float*>(base + oQc1);
+  c->q_c2 = reinterpret_cast<float*>(base + oQc2);
+  c->W_KU = base + oWKU;
+  c->m_c1 = reinterpret_cast<float*>(base + oMc1);
+  c->m_c2 = reinterpret_cast<float*>(base + oMc2);
+  c->W1 = base + oW1;
+  c->b1 = reinterpret_cast<float*>(base + oB1);
+  c->W_c2 = base + oWc2;
+  c->b_c2 = reinterpret_cast<float*>(base + oBc2);
+  c->w_g2 = reinterpret_cast<float*>(base + oWg2);
+  c->rms_w = p->rms_w ? reinterpret_cast<float*>(base + oRms) : nullptr;
+  c->err = reinterpret_cast<uint32_t*>(base + oErr);
+  fovea_status st = hipMemsetAsync(c->err, 0, 4, stream) == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+  if (st == FOVEA_OK) st = c->bf16 ? pack_weights<bf16_t>(c, p, stream) : pack_weights<float>(c, p, stream);
+  if (st == FOVEA_OK && hipStreamSynchronize(stream) != hipSuccess) st = FOVEA_ERR_DEVICE;
+  if (st != FOVEA_OK) {
+    (void)hipFree(c->block);
+    delete c;
+    return st;
+  }
+  *out = c;
+  return FOVEA_OK;
+}
+
+void fovea_destroy(fovea_ctx* c) {
+  if (c == nullptr) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  (void)hipSetDevice(c->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(c->block);
+  if (c->build_stats) (void)hipFree(c->build_stats);
+  (void)hipSetDevice(cur);
+  delete c;
+}
+
+fovea_status fovea_build_memory(fovea_ctx* c, int64_t n_rows, const void* V, void* keys,
+                                void* values, hipStream_t stream) {
+  if (c == nullptr || n_rows < 0) return FOVEA_ERR_INVALID_ARG;
+  if (n_rows == 0) return FOVEA_OK;
+  if (V == nullptr || keys == nullptr || values == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (n_rows > (int64_t{1} << 30)) return FOVEA_ERR_UNSUPPORTED;
+  if (!aligned16(V) || !aligned16(keys) || !aligned16(values)) return FOVEA_ERR_INVALID_ARG;
+  const size_t nv = static_cast<size_t>(n_rows) * c->dims.d_v * c->es;
+  const size_t nk = static_cast<size_t>(n_rows) * c->dims.d_m * c->es;
+  if (overlaps(keys, nk, V, nv) || overlaps(values, nk, V, nv) || overlaps(keys, nk, values, nk))
+    return FOVEA_ERR_INVALID_ARG;
+  if (c->build_stats_rows < n_rows) {
+    if (c->build_stats) {
+      if (hipStreamSynchronize(stream) != hipSuccess) return FOVEA_ERR_DEVICE;
+      (void)hipFree(c->build_stats);
+      c->build_stats = nullptr;
+      c->build_stats_rows = 0;
+    }
+    if (hipMalloc(&c->build_stats, static_cast<size_t>(n_rows) * sizeof(float2)) != hipSuccess)
+      return FOVEA_ERR_DEVICE;
+    c->build_stats_rows = n_rows;
+  }
+  const int n = static_cast<int>(n_rows);
+  return c->bf16 ? run_build<bf16_t>(c, n, V, keys, values, stream)
+                 : run_build<float>(c, n, V, keys, values, stream);
+}
+
+size_t fovea_retrieve_fuse_workspace(const fovea_ctx* c, int32_t n_nodes_total, int32_t m_max,
+                                     int32_t k_max) {
+  if (c == nullptr || n_nodes_total < 0 || m_max < 0 || k_max < 1) return 0;
+  return ws_layout(c->dims, n_nodes_total, m_max).total;
+}
+
+fovea_status fovea_retrieve_fuse(fovea_ctx* c, int32_t B, const int64_t* mem_off,
+                                 int64_t n_mem_total, int32_t m_max, const void* keys,
+                                 const void* values, const uint8_t* valid,
+                                 const int32_t* node_off, int32_t n_nodes_total, int32_t t_max,
+                                 const void* h, const int32_t* depth, const float* tau,
+                                 int32_t k_min, int32_t k_max, void* h_out, int32_t* k_out,
+                                 int32_t* idx_out, float* gate_out, float* mass_out, float* r_out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (c == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (B < 0 || n_mem_total < 0 || m_max < 0 || n_nodes_total < 0 || t_max < 0) return FOVEA_ERR_INVALID_ARG;
+  if (k_max < 1 || k_min < 0 || k_min > k_max) return FOVEA_ERR_INVALID_ARG;
+  if (n_nodes_total > 0 && (B == 0 || t_max == 0)) return FOVEA_ERR_INVALID_ARG;
+  if (n_nodes_total == 0) return FOVEA_OK;
+  if (mem_off == nullptr || node_off == nullptr || h == nullptr || depth == nullptr ||
+      tau == nullptr || h_out == nullptr || workspace == nullptr)
+    return FOVEA_ERR_INVALID_ARG;
+  if (n_mem_total > 0 && (keys == nullptr || values == nullptr)) return FOVEA_ERR_INVALID_ARG;
+  if (m_max > kMaxM || k_max > kMaxKmax) return FOVEA_ERR_UNSUPPORTED;
+  if (n_mem_total > (int64_t{1} << 40)) return FOVEA_ERR_UNSUPPORTED;
+  if (!aligned16(keys) || !aligned16(values) || !aligned16(h) || !aligned16(h_out))
+    return FOVEA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return FOVEA_ERR_WORKSPACE;
+  const fovea_dims& D = c->dims;
+  const WsLayout L = ws_layout(D, n_nodes_total, m_max);
+  if (workspace_bytes < L.total) return FOVEA_ERR_WORKSPACE;
+  const size_t nh = static_cast<size_t>(n_nodes_total) * D.d * c->es;
+  const size_t nk = static_cast<size_t>(n_mem_total) * D.d_m * c->es;
+  if (overlaps(h_out, nh, h, nh) || overlaps(h_out, nh, keys, nk) || overlaps(h_out, nh, values, nk) ||
+      overlaps(h_out, nh, workspace, L.total))
+    return FOVEA_ERR_INVALID_ARG;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
+
+  RFArgs a;
+  a.B = B;
+  a.mem_off = mem_off;
+  a.n_mem = n_mem_total;
+  a.m_max = m_max;
+  a.keys = keys;
+  a.values = values;
+  a.valid = valid;
+  a.node_off = node_off;
+  a.n = n_nodes_total;
+  a.t_max = t_max;
+  a.h = h;
+  a.depth = depth;
+  a.tau = tau;
+  a.k_min = k_min;
+  a.k_max = k_max;
+  a.h_out = h_out;
+  a.k_out = k_out;
+  a.idx_out = idx_out;
+  a.gate_out = gate_out;
+  a.mass_out = mass_out;
+  a.r_out = r_out;
+  a.ws = static_cast<char*>(workspace);
+  return c->bf16 ? run_retrieve_fuse<bf16_t>(c, a, stream) : run_retrieve_fuse<float>(c, a, stream);
+}
+
+fovea_status fovea_last_error(fovea_ctx* c, hipStream_t stream, uint32_t* bits) {
+  if (c == nullptr) return FOVEA_ERR_INVALID_ARG;
+  uint32_t v = 0;
+  if (hipStreamSynchronize(stream) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (hipMemcpy(&v, c->err, 4, hipMemcpyDeviceToHost) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (v != 0 && hipMemset(c->err, 0, 4) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (bits) *bits = v;
+  return v ? FOVEA_ERR_DATA : FOVEA_OK;
+}
+
+}  // extern "C"

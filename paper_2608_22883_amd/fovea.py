@@ -1,0 +1,259 @@
+"""ctypes binding of libfovea.so (the C ABI in include/fovea.h).
+
+Argument marshalling only: torch tensors supply device pointers and torch's current
+stream supplies the HIP stream; every step of the computation runs in the library's
+HIP kernels.  Importing this module fails loudly if the library has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libfovea.so")
+
+FOVEA_OK = 0
+FOVEA_ERR_INVALID_ARG = 1
+FOVEA_ERR_UNSUPPORTED = 2
+FOVEA_ERR_WORKSPACE = 3
+FOVEA_ERR_DEVICE = 4
+FOVEA_ERR_DATA = 5
+FOVEA_F32 = 0
+FOVEA_BF16 = 1
+
+FOVEA_DATA_BAD_NODE_OFFSETS = 0x1
+FOVEA_DATA_BAD_MEM_OFFSETS = 0x2
+FOVEA_DATA_BAD_DEPTH = 0x4
+FOVEA_DATA_BAD_TAU = 0x8
+
+FOVEA_MAX_M = 16384
+FOVEA_MAX_KMAX = 1024
+
+EXPORTED = [
+    "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
+    "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
+    "fovea_last_error",
+]
+
+
+class FoveaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {fovea_status_str(status)} (status {status})")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("d_v", ctypes.c_int32), ("d_m", ctypes.c_int32),
+                ("d_c", ctypes.c_int32), ("n_depth", ctypes.c_int32), ("dtype", ctypes.c_int),
+                ("ln_eps", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+
+
+PARAM_TENSORS = ["mem_ln_g", "mem_ln_b", "W_K", "W_U", "q_ln_g", "q_ln_b", "E_dep", "W_Q",
+                 "W_c1", "b_c1", "W_c2", "b_c2", "W_g1", "b_g1", "w_g2"]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_TENSORS] + [
+        ("b_g2", ctypes.c_float), ("rms_w", ctypes.c_void_p)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.fovea_abi_version.restype = ctypes.c_int
+    lib.fovea_abi_version.argtypes = []
+    lib.fovea_status_str.restype = ctypes.c_char_p
+    lib.fovea_status_str.argtypes = [ctypes.c_int]
+    lib.fovea_create.restype = ctypes.c_int
+    lib.fovea_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(Dims), ctypes.POINTER(Params), vp]
+    lib.fovea_destroy.restype = None
+    lib.fovea_destroy.argtypes = [vp]
+    lib.fovea_build_memory.restype = ctypes.c_int
+    lib.fovea_build_memory.argtypes = [vp, i64, vp, vp, vp, vp]
+    lib.fovea_retrieve_fuse_workspace.restype = sz
+    lib.fovea_retrieve_fuse_workspace.argtypes = [vp, i32, i32, i32]
+    lib.fovea_retrieve_fuse.restype = ctypes.c_int
+    lib.fovea_retrieve_fuse.argtypes = [
+        vp, i32, vp, i64, i32, vp, vp, vp, vp, i32, i32, vp, vp, vp, i32, i32,
+        vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.fovea_last_error.restype = ctypes.c_int
+    lib.fovea_last_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
+    return lib
+
+
+lib = _load()
+
+
+def fovea_abi_version() -> int:
+    return lib.fovea_abi_version()
+
+
+def fovea_status_str(status: int) -> str:
+    return lib.fovea_status_str(status).decode()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr(t: torch.Tensor | None, dtype=None, name: str = "") -> int | None:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _check(status: int, where: str):
+    if status != FOVEA_OK:
+        raise FoveaError(status, where)
+
+
+def storage_dtype(dtype: int) -> torch.dtype:
+    return torch.bfloat16 if dtype == FOVEA_BF16 else torch.float32
+
+
+def fovea_create(dims: Dims, params: dict, b_g2: float, stream=None) -> int:
+    """params: the PARAM_TENSORS (and optional "rms_w") as device tensors in the storage
+    dtype.  Returns the opaque context handle."""
+    dt = storage_dtype(dims.dtype)
+    P = Params()
+    for n in PARAM_TENSORS:
+        setattr(P, n, _ptr(params[n], dt, n))
+    P.b_g2 = float(b_g2)
+    P.rms_w = _ptr(params.get("rms_w"), dt, "rms_w")
+    ctx = ctypes.c_void_p()
+    _check(lib.fovea_create(ctypes.byref(ctx), ctypes.byref(dims), ctypes.byref(P), _stream(stream)),
+           "fovea_create")
+    return ctx.value
+
+
+def fovea_destroy(ctx: int) -> None:
+    lib.fovea_destroy(ctx)
+
+
+def fovea_build_memory(ctx: int, V: torch.Tensor, keys: torch.Tensor, values: torch.Tensor,
+                       stream=None) -> None:
+    _check(lib.fovea_build_memory(ctx, V.shape[0], _ptr(V, None, "V"), _ptr(keys, V.dtype, "keys"),
+                                  _ptr(values, V.dtype, "values"), _stream(stream)),
+           "fovea_build_memory")
+
+
+def fovea_retrieve_fuse_workspace(ctx: int, n_nodes_total: int, m_max: int, k_max: int) -> int:
+    return lib.fovea_retrieve_fuse_workspace(ctx, n_nodes_total, m_max, k_max)
+
+
+def fovea_retrieve_fuse(ctx: int, B: int, mem_off, n_mem_total: int, m_max: int, keys, values,
+                        valid, node_off, n_nodes_total: int, t_max: int, h, depth, tau,
+                        k_min: int, k_max: int, h_out, k_out=None, idx_out=None, gate_out=None,
+                        mass_out=None, r_out=None, workspace=None, stream=None) -> None:
+    """Same arguments as the C entry point; tensors stand for device pointers."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.fovea_retrieve_fuse(
+        ctx, B, _ptr(mem_off, torch.int64, "mem_off"), n_mem_total, m_max,
+        _ptr(keys, h.dtype, "keys"), _ptr(values, h.dtype, "values"),
+        _ptr(valid, torch.uint8, "valid"), _ptr(node_off, torch.int32, "node_off"),
+        n_nodes_total, t_max, _ptr(h, None, "h"), _ptr(depth, torch.int32, "depth"),
+        _ptr(tau, torch.float32, "tau"), k_min, k_max, _ptr(h_out, h.dtype, "h_out"),
+        _ptr(k_out, torch.int32, "k_out"), _ptr(idx_out, torch.int32, "idx_out"),
+        _ptr(gate_out, torch.float32, "gate_out"), _ptr(mass_out, torch.float32, "mass_out"),
+        _ptr(r_out, torch.float32, "r_out"), _ptr(workspace, None, "workspace"), ws_bytes,
+        _stream(stream))
+    _check(st, "fovea_retrieve_fuse")
+
+
+def fovea_last_error(ctx: int, stream=None) -> tuple[int, int]:
+    bits = ctypes.c_uint32(0)
+    st = lib.fovea_last_error(ctx, _stream(stream), ctypes.byref(bits))
+    return st, bits.value
+
+
+# ------------------------------------------------------------------------------------
+# convenience wrapper used by the tests and the benchmark
+# ------------------------------------------------------------------------------------
+
+
+@dataclass
+class Outputs:
+    h_out: torch.Tensor
+    k: torch.Tensor
+    idx: torch.Tensor
+    gate: torch.Tensor
+    mass: torch.Tensor
+    r: torch.Tensor
+
+
+class Fovea:
+    """Owns one context, its device weight copies and a workspace."""
+
+    def __init__(self, dims: dict, weights: dict, device="cuda", stream=None):
+        self.dims = Dims(dims["d"], dims["d_v"], dims["d_m"], dims["d_c"], dims["n_depth"],
+                         dims["dtype"], dims["ln_eps"], dims["rms_eps"])
+        self.dtype = storage_dtype(dims["dtype"])
+        self.device = torch.device(device)
+        self.params = {}
+        for n in PARAM_TENSORS + ["rms_w"]:
+            v = weights.get(n)
+            if v is None:
+                continue
+            self.params[n] = torch.as_tensor(v).to(device=self.device, dtype=self.dtype).contiguous()
+        self.ctx = fovea_create(self.dims, self.params, float(weights["b_g2"]), stream)
+        self.workspace = None
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            fovea_destroy(self.ctx)
+            self.ctx = None
+
+    __del__ = close
+
+    def ensure_workspace(self, n_nodes_total: int, m_max: int, k_max: int) -> torch.Tensor:
+        need = fovea_retrieve_fuse_workspace(self.ctx, n_nodes_total, m_max, k_max)
+        if self.workspace is None or self.workspace.numel() < need:
+            self.workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        return self.workspace
+
+    def build_memory(self, V: torch.Tensor, stream=None):
+        keys = torch.empty(V.shape[0], self.dims.d_m, dtype=V.dtype, device=V.device)
+        values = torch.empty_like(keys)
+        fovea_build_memory(self.ctx, V, keys, values, stream)
+        return keys, values
+
+    def alloc_outputs(self, n: int, k_max: int, d: int, d_m: int) -> Outputs:
+        dev = self.device
+        return Outputs(
+            h_out=torch.empty(n, d, dtype=self.dtype, device=dev),
+            k=torch.empty(n, dtype=torch.int32, device=dev),
+            idx=torch.empty(n, k_max, dtype=torch.int32, device=dev),
+            gate=torch.empty(n, dtype=torch.float32, device=dev),
+            mass=torch.empty(n, dtype=torch.float32, device=dev),
+            r=torch.empty(n, d_m, dtype=torch.float32, device=dev))
+
+    def retrieve_fuse(self, inp: dict, out: Outputs | None = None, debug: bool = True,
+                      stream=None) -> Outputs:
+        """inp: device tensors mem_off, keys, values, valid (or None), node_off, h, depth,
+        tau and host ints m_max, t_max, k_min, k_max."""
+        n = inp["h"].shape[0]
+        k_max = inp["k_max"]
+        if out is None:
+            out = self.alloc_outputs(n, k_max, self.dims.d, self.dims.d_m)
+        ws = self.ensure_workspace(n, inp["m_max"], k_max)
+        fovea_retrieve_fuse(
+            self.ctx, inp["mem_off"].numel() - 1, inp["mem_off"], inp["keys"].shape[0],
+            inp["m_max"], inp["keys"], inp["values"], inp.get("valid"), inp["node_off"], n,
+            inp["t_max"], inp["h"], inp["depth"], inp["tau"], inp["k_min"], k_max, out.h_out,
+            out.k if debug else None, out.idx if debug else None, out.gate if debug else None,
+            out.mass if debug else None, out.r if debug else None, ws, stream)
+        return out
