@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Throughput of one draft step of FOVEA's retrieval + fusion on one MI355X.
+
+A step is one fovea_retrieve_fuse call over the whole batch: query projection, scoring
+of every valid key, cumulative-mass selection, renormalised gather, correction MLPs,
+gated residual and RMSNorm.  Default workload: the batched serving shape (32 requests,
+each with its own 576-entry memory, 60 draft-tree nodes per request, d = 4096,
+d_m = 1024, k_max = 64, tau per request in [0.6, 0.95]), synthetic seeded inputs.
+
+Protocol: inputs are resident in HBM; the timed loop rotates over several copies of
+the inputs (more bytes than the 256 MB Infinity Cache) so each step reads its keys,
+values and hidden states from HBM; W warm-up steps, then exactly K steps between two
+HIP events after a device synchronisation.  A second, profiled pass brackets every
+kernel with HIP events for the per-kernel roofline.  The fp64 oracle is timed on the
+host cores on a bounded sample as the CPU baseline.
+
+Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0    # dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3     # dense fp32
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="batched_b32")
+    ap.add_argument("--copies", type=int, default=6, help="input copies rotated in the timed loop")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def kernel_model(wl, case, union_rows, k_sum):
+    """Algorithmic bytes and flops per launch of each kernel (storage dtype es)."""
+    import numpy as np
+
+    es = 2 if wl.dtype == "bf16" else 4
+    n, d, d_m, d_c = case.n_nodes, wl.d, wl.d_m, wl.d_c
+    Ms = np.diff(case.mem_off).astype(np.int64)
+    Ts = np.diff(case.node_off).astype(np.int64)
+    pairs = int((Ms * Ts).sum())
+    n_mem = int(Ms.sum())
+    k = {}
+    k["row_stats"] = dict(bytes=n * d * es + n * 8, flops=3 * n * d)
+    k["q_proj"] = dict(bytes=n * d * es + d_m * d * es + n * d_m * 4, flops=2 * n * d * d_m)
+    k["score"] = dict(bytes=n_mem * d_m * es + n * d_m * 4 + pairs * 4, flops=2 * pairs * d_m)
+    k["select_gather"] = dict(bytes=pairs * 4 + union_rows * d_m * es + n * d_m * es,
+                              flops=2 * int(k_sum) * d_m)
+    k["corr1"] = dict(bytes=n * (d + d_m) * es + 2 * d_c * (d + d_m) * es + n * d_c * es,
+                      flops=2 * n * (d + d_m) * 2 * d_c)
+    k["corr2"] = dict(bytes=n * d_c * es + d * d_c * es + 2 * n * d * es, flops=2 * n * d_c * d)
+    k["rms"] = dict(bytes=2 * n * d * es, flops=3 * n * d)
+    # the retrieval as one operation: every key, q, the selected value rows, r
+    retrieval = dict(bytes=n_mem * d_m * es + n * d_m * 4 + union_rows * d_m * es + n * d_m * es,
+                     flops=2 * pairs * d_m)
+    return k, retrieval
+
+
+def cpu_baseline(case, budget_s):
+    """The fp64 oracle, as it stands, on the host cores: whole steps of the same workload
+    repeated until the time budget is used (at least one)."""
+    import numpy as np  # noqa: F401
+
+    import oracle
+    from threadpoolctl import threadpool_info
+
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        oracle.retrieve_fuse(case.weights, case.mem_off, case.keys, case.values, case.valid,
+                             case.node_off, case.h, case.depth, case.tau, case.k_min, case.k_max,
+                             gain_rounding="bf16" if case.workload.dtype == "bf16" else None)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or el / reps * (reps + 1) > 2.5 * budget_s:
+            break
+    return dict(value=case.n_nodes * reps / el, unit="states/s", cores=int(threads), kind="oracle",
+                sample=f"{reps} full step(s) of the same workload ({case.n_nodes} draft states each), "
+                       f"{el:.1f} s wall, fp64 NumPy, BLAS threads={threads}, "
+                       f"affinity cpus={len(os.sched_getaffinity(0))}")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the retrieval of each request is independent, "
+              "so more GPUs would each run this same single-GPU step on their share of the "
+              "requests; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_22883_amd import Fovea, fovea_profile, fovea_profile_read
+    from synth import WORKLOADS, make_case
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = WORKLOADS[args.workload]
+    log(f"[bench] generating {wl.name} ...")
+    case = make_case(wl)
+    W = case.weights
+    dev = torch.device("cuda:0")
+    dims = dict(d=wl.d, d_v=wl.d, d_m=wl.d_m, d_c=wl.d_c, n_depth=wl.n_depth,
+                dtype=1 if wl.dtype == "bf16" else 0, ln_eps=W["ln_eps"], rms_eps=W["rms_eps"])
+    fv = Fovea(dims, W, device=dev)
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+
+    def dev_t(x, d=dt):
+        return torch.tensor(np.asarray(x), dtype=d, device=dev)
+
+    base = dict(mem_off=torch.tensor(case.mem_off, dtype=torch.int64, device=dev),
+                keys=dev_t(case.keys), values=dev_t(case.values), valid=None,
+                node_off=torch.tensor(case.node_off, dtype=torch.int32, device=dev),
+                h=dev_t(case.h), depth=torch.tensor(case.depth, dtype=torch.int32, device=dev),
+                tau=dev_t(case.tau, torch.float32), m_max=case.m_max, t_max=case.t_max,
+                k_min=case.k_min, k_max=case.k_max)
+    # copies at distinct addresses so that consecutive steps cannot hit in the 256 MB MALL
+    sets = [base] + [dict(base, keys=base["keys"].clone(), values=base["values"].clone(),
+                          h=base["h"].clone()) for _ in range(args.copies - 1)]
+    per_set = sum(base[k].numel() * base[k].element_size() for k in ("keys", "values", "h"))
+    out = fv.alloc_outputs(case.n_nodes, case.k_max, wl.d, wl.d_m)
+
+    # one debug run: selected sets (for the algorithmic gather bytes) and a sanity check
+    fv.retrieve_fuse(base, out, debug=True)
+    torch.cuda.synchronize()
+    K = out.k.cpu().numpy()
+    idx = out.idx.cpu().numpy()
+    union_rows = 0
+    for b in range(wl.B):
+        t0, t1 = case.node_off[b], case.node_off[b + 1]
+        sel = idx[t0:t1]
+        union_rows += len(np.unique(sel[sel >= 0]))
+    log(f"[bench] K min/median/max {K.min()}/{np.median(K)}/{K.max()}, union rows {union_rows}")
+
+    # whole-step timing
+    for i in range(args.warmup):
+        fv.retrieve_fuse(sets[i % len(sets)], out, debug=False)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        fv.retrieve_fuse(sets[i % len(sets)], out, debug=False)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"[bench] {args.steps} steps: {ms * 1e3:.1f} us/step")
+
+    # per-kernel timing (events around each kernel, on the library's stream)
+    fovea_profile(fv.ctx, True)
+    for i in range(args.steps):
+        fv.retrieve_fuse(sets[i % len(sets)], out, debug=False)
+    torch.cuda.synchronize()
+    prof = fovea_profile_read(fv.ctx)
+    fovea_profile(fv.ctx, False)
+
+    kmodel, retrieval = kernel_model(wl, case, union_rows, int(K.sum()))
+    kernels = []
+    for name, (tot, cnt) in prof.items():
+        avg_ms = tot / cnt
+        m = kmodel.get(name, dict(bytes=0, flops=0))
+        gbs = m["bytes"] / (avg_ms * 1e-3) / 1e9
+        tfl = m["flops"] / (avg_ms * 1e-3) / 1e12
+        peak_fl = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+        mfma = name in ("q_proj", "corr1", "corr2")
+        kernels.append(dict(
+            name=name, avg_us=round(avg_ms * 1e3, 2), launches=cnt, alg_bytes=m["bytes"],
+            alg_flops=m["flops"], GBs=round(gbs, 1), TFLOPs=round(tfl, 2),
+            bound="mfma" if mfma else "hbm",
+            frac=round((tfl / peak_fl) if mfma else (gbs / PEAK_HBM_GBS), 4)))
+        log(f"[bench] {name:14s} {avg_ms * 1e3:8.2f} us  {gbs:8.1f} GB/s  {tfl:7.2f} TFLOP/s")
+    kernels.sort(key=lambda k: -k["avg_us"])
+    dom = kernels[0]
+    if dom["bound"] == "mfma":
+        roof = dict(bound="mfma", achieved=dom["TFLOPs"],
+                    peak=PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS,
+                    unit="TFLOP/s", frac=dom["frac"], traffic=None, kernel=dom["name"])
+    else:
+        roof = dict(bound="hbm", achieved=dom["GBs"], peak=PEAK_HBM_GBS, unit="GB/s",
+                    frac=dom["frac"], traffic=None, kernel=dom["name"])
+    ret_us = sum(k["avg_us"] for k in kernels if k["name"] in ("score", "select_gather"))
+    ret_gbs = retrieval["bytes"] / (ret_us * 1e-6) / 1e9 if ret_us else 0.0
+
+    line = dict(
+        metric="draft states/sec for retrieve+fuse (M=576, d=4096); % of peak HBM GB/s",
+        value=round(case.n_nodes / (ms * 1e-3), 1), unit="states/s", n_gpus=1,
+        steps=args.steps, warmup=args.warmup, ms_per_step=round(ms, 5), higher_is_better=True,
+        scaling="weak", vs_baseline=None, dtype=wl.dtype, data="synthetic",
+        config=dict(workload=wl.name, description=wl.description, B=wl.B, T=wl.T, M=wl.M,
+                    d=wl.d, d_m=wl.d_m, d_c=wl.d_c, k_max=wl.k_max,
+                    states_per_step=case.n_nodes, input_copies=len(sets),
+                    rotated_bytes=per_set * len(sets)),
+        roofline=roof,
+        retrieval=dict(kernels=["score", "select_gather"], us=round(ret_us, 2),
+                       alg_bytes=retrieval["bytes"], GBs=round(ret_gbs, 1),
+                       frac=round(ret_gbs / PEAK_HBM_GBS, 4)),
+        kernels=kernels,
+        K=dict(min=int(K.min()), median=float(np.median(K)), max=int(K.max()),
+               union_value_rows=int(union_rows)),
+    )
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host ...")
+        line["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    fv.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -165,6 +165,17 @@ fovea_status fovea_retrieve_fuse(fovea_ctx* ctx, int32_t B, const int64_t* mem_o
  * FOVEA_ERR_DEVICE on a HIP error, else FOVEA_OK. */
 fovea_status fovea_last_error(fovea_ctx* ctx, hipStream_t stream, uint32_t* bits);
 
+/* Diagnostics: per-kernel timing with HIP events.  While enabled, every kernel that
+ * fovea_retrieve_fuse or fovea_build_memory launches is bracketed by two HIP events on
+ * the call's stream (this adds event packets between the kernels, so time whole calls
+ * with profiling off).  fovea_profile_read waits for the recorded events, writes up to
+ * max_kernels entries (kernel name, summed milliseconds, launch count; names are
+ * static strings owned by the library) and forgets what it read.  Returns the number
+ * of entries written, or -1 on an error. */
+fovea_status fovea_profile(fovea_ctx* ctx, int32_t enable);
+int32_t fovea_profile_read(fovea_ctx* ctx, int32_t max_kernels, const char** names,
+                           float* total_ms, int32_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstring>
 #include <new>
+#include <vector>
 
 #include "fovea.h"
 #include "correct_kernels.hpp"
@@ -35,6 +36,14 @@ struct fovea_ctx {
   uint32_t* err;  // sticky device-data error bits
   float2* build_stats;
   int64_t build_stats_rows;
+  // diagnostics: HIP event pairs around each launched kernel
+  bool prof;
+  struct ProfRec {
+    int slot;
+    hipEvent_t e0, e1;
+  };
+  std::vector<ProfRec> prof_recs;
+  std::vector<hipEvent_t> prof_pool;
 };
 
 namespace {
@@ -92,6 +101,42 @@ bool dims_supported(const fovea_dims* d) {
     if ((call) != hipSuccess) return FOVEA_ERR_DEVICE;    \
   } while (0)
 
+enum KernelSlot { kRowStats, kQProj, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kNumSlots };
+const char* const kSlotNames[kNumSlots] = {"row_stats", "q_proj", "score", "select_gather",
+                                           "corr1", "corr2", "rms", "mem_row_stats", "mem_proj"};
+
+hipEvent_t prof_event(fovea_ctx* c) {
+  if (!c->prof_pool.empty()) {
+    hipEvent_t e = c->prof_pool.back();
+    c->prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Brackets one kernel launch with events when profiling is on.
+struct ProfScope {
+  fovea_ctx* c;
+  int slot;
+  hipStream_t s;
+  hipEvent_t e0 = nullptr;
+  ProfScope(fovea_ctx* c_, int slot_, hipStream_t s_) : c(c_), slot(slot_), s(s_) {
+    if (c->prof && (e0 = prof_event(c)) != nullptr) (void)hipEventRecord(e0, s);
+  }
+  ~ProfScope() {
+    if (e0 == nullptr) return;
+    hipEvent_t e1 = prof_event(c);
+    if (e1 == nullptr) {
+      c->prof_pool.push_back(e0);
+      return;
+    }
+    (void)hipEventRecord(e1, s);
+    c->prof_recs.push_back({slot, e0, e1});
+  }
+};
+
 template <typename T>
 fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
   const fovea_dims& D = c->dims;
@@ -137,16 +182,22 @@ fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
 template <typename T>
 fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* values, hipStream_t s) {
   const fovea_dims& D = c->dims;
-  hipLaunchKernelGGL(row_stats_kernel<T>, dim3((n + 3) / 4), dim3(256), 0, s, n,
-                     static_cast<const T*>(V), D.d_v, D.ln_eps, c->build_stats,
-                     static_cast<const int32_t*>(nullptr), 0, static_cast<const int32_t*>(nullptr),
-                     0, 0, static_cast<const float*>(nullptr), static_cast<int32_t*>(nullptr),
-                     c->err);
+  {
+    ProfScope ps(c, kMemStats, s);
+    hipLaunchKernelGGL(row_stats_kernel<T>, dim3((n + 3) / 4), dim3(256), 0, s, n,
+                       static_cast<const T*>(V), D.d_v, D.ln_eps, c->build_stats,
+                       static_cast<const int32_t*>(nullptr), 0, static_cast<const int32_t*>(nullptr),
+                       0, 0, static_cast<const float*>(nullptr), static_cast<int32_t*>(nullptr),
+                       c->err);
+  }
   using C = GemmCfg<T, kCorrWM, kCorrWN, kCorrTM, kCorrTN>;
   const dim3 grid((n + C::BM - 1) / C::BM, (2 * D.d_m + C::BN - 1) / C::BN);
-  hipLaunchKernelGGL(mem_proj_kernel<T>, grid, dim3(C::NT), 0, s, n, static_cast<const T*>(V),
-                     D.d_v, static_cast<const T*>(c->W_KU), D.d_m, c->build_stats, c->m_c1,
-                     c->m_c2, static_cast<T*>(keys), static_cast<T*>(values));
+  {
+    ProfScope ps(c, kMemProj, s);
+    hipLaunchKernelGGL(mem_proj_kernel<T>, grid, dim3(C::NT), 0, s, n, static_cast<const T*>(V),
+                       D.d_v, static_cast<const T*>(c->W_KU), D.d_m, c->build_stats, c->m_c1,
+                       c->m_c2, static_cast<T*>(keys), static_cast<T*>(values));
+  }
   FOVEA_HIP(hipGetLastError());
   return FOVEA_OK;
 }
@@ -192,17 +243,24 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   const int row_blocks = (a.n + C::BM - 1) / C::BM;
 
   // 1. LayerNorm statistics of h, node -> request map, depth / tau / offset checks
-  hipLaunchKernelGGL(row_stats_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, h, D.d,
-                     D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
-                     node_req, c->err);
+  {
+    ProfScope ps(c, kRowStats, s);
+    hipLaunchKernelGGL(row_stats_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, h, D.d,
+                       D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
+                       node_req, c->err);
+  }
   // 2. q = W_Q (LN(h) + E_dep[l])
-  hipLaunchKernelGGL(q_proj_kernel<T>, dim3(row_blocks, (D.d_m + C::BN - 1) / C::BN), dim3(C::NT),
-                     0, s, a.n, h, D.d, static_cast<const T*>(c->W_Q), D.d_m, stats, a.depth,
-                     node_req, D.n_depth, c->q_c1, c->q_c2, q);
+  {
+    ProfScope ps(c, kQProj, s);
+    hipLaunchKernelGGL(q_proj_kernel<T>, dim3(row_blocks, (D.d_m + C::BN - 1) / C::BN),
+                       dim3(C::NT), 0, s, a.n, h, D.d, static_cast<const T*>(c->W_Q), D.d_m,
+                       stats, a.depth, node_req, D.n_depth, c->q_c1, c->q_c2, q);
+  }
   // 3. scores for every (node, key) of each request
   if (a.m_max > 0) {
     const int tiles = (a.m_max + 63) / 64;
     const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.d_m)));
+    ProfScope ps(c, kScore, s);
     hipLaunchKernelGGL(score_kernel<T>, dim3(a.B * tiles), dim3(256), 0, s, a.B, a.mem_off,
                        a.n_mem, a.m_max, a.node_off, a.n, a.t_max, static_cast<const T*>(a.keys),
                        D.d_m, static_cast<const T*>(q), scale, S);
@@ -231,20 +289,31 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                   static_cast<int>(sel_smem)));
-  hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
+  {
+    ProfScope ps(c, kSelect, s);
+    hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
+  }
   // 5. correction layer 1 (+ gate logit partials)
-  hipLaunchKernelGGL(corr1_kernel<T>, dim3(row_blocks, (2 * D.d_c + C::BN - 1) / C::BN),
-                     dim3(C::NT), 0, s, a.n, h, D.d, rT, D.d_m, static_cast<const T*>(c->W1),
-                     c->b1, D.d_c, c->w_g2, a_c, gate_part);
+  {
+    ProfScope ps(c, kCorr1, s);
+    hipLaunchKernelGGL(corr1_kernel<T>, dim3(row_blocks, (2 * D.d_c + C::BN - 1) / C::BN),
+                       dim3(C::NT), 0, s, a.n, h, D.d, rT, D.d_m, static_cast<const T*>(c->W1),
+                       c->b1, D.d_c, c->w_g2, a_c, gate_part);
+  }
   // 6. correction layer 2, gate, residual (+ RMS partials)
   T* h_out = static_cast<T*>(a.h_out);
-  hipLaunchKernelGGL(corr2_kernel<T>, dim3(row_blocks, (D.d + C::BN - 1) / C::BN), dim3(C::NT),
-                     0, s, a.n, a_c, D.d_c, static_cast<const T*>(c->W_c2), D.d, c->b_c2,
-                     gate_part, c->b_g2, h, h_out, a.gate_out, rms_part, c->rms_w ? 1 : 0);
+  {
+    ProfScope ps(c, kCorr2, s);
+    hipLaunchKernelGGL(corr2_kernel<T>, dim3(row_blocks, (D.d + C::BN - 1) / C::BN), dim3(C::NT),
+                       0, s, a.n, a_c, D.d_c, static_cast<const T*>(c->W_c2), D.d, c->b_c2,
+                       gate_part, c->b_g2, h, h_out, a.gate_out, rms_part, c->rms_w ? 1 : 0);
+  }
   // 7. RMSNorm
-  if (c->rms_w)
+  if (c->rms_w) {
+    ProfScope ps(c, kRms, s);
     hipLaunchKernelGGL(rms_kernel<T>, dim3(a.n), dim3(256), 0, s, a.n, D.d, rms_part, c->rms_w,
                        D.rms_eps, h_out);
+  }
   FOVEA_HIP(hipGetLastError());
   return FOVEA_OK;
 }
@@ -343,6 +412,11 @@ void fovea_destroy(fovea_ctx* c) {
   (void)hipDeviceSynchronize();
   (void)hipFree(c->block);
   if (c->build_stats) (void)hipFree(c->build_stats);
+  for (auto& r : c->prof_recs) {
+    (void)hipEventDestroy(r.e0);
+    (void)hipEventDestroy(r.e1);
+  }
+  for (hipEvent_t e : c->prof_pool) (void)hipEventDestroy(e);
   (void)hipSetDevice(cur);
   delete c;
 }
@@ -448,6 +522,40 @@ fovea_status fovea_last_error(fovea_ctx* c, hipStream_t stream, uint32_t* bits) 
   if (v != 0 && hipMemset(c->err, 0, 4) != hipSuccess) return FOVEA_ERR_DEVICE;
   if (bits) *bits = v;
   return v ? FOVEA_ERR_DATA : FOVEA_OK;
+}
+
+fovea_status fovea_profile(fovea_ctx* c, int32_t enable) {
+  if (c == nullptr) return FOVEA_ERR_INVALID_ARG;
+  c->prof = enable != 0;
+  return FOVEA_OK;
+}
+
+int32_t fovea_profile_read(fovea_ctx* c, int32_t max_kernels, const char** names, float* total_ms,
+                           int32_t* launches) {
+  if (c == nullptr || max_kernels < 0) return -1;
+  float ms[kNumSlots] = {};
+  int32_t cnt[kNumSlots] = {};
+  bool ok = true;
+  for (auto& r : c->prof_recs) {
+    float t = 0.f;
+    if (hipEventSynchronize(r.e1) != hipSuccess || hipEventElapsedTime(&t, r.e0, r.e1) != hipSuccess)
+      ok = false;
+    ms[r.slot] += t;
+    cnt[r.slot] += 1;
+    c->prof_pool.push_back(r.e0);
+    c->prof_pool.push_back(r.e1);
+  }
+  c->prof_recs.clear();
+  if (!ok) return -1;
+  int32_t w = 0;
+  for (int i = 0; i < kNumSlots && w < max_kernels; ++i) {
+    if (cnt[i] == 0) continue;
+    if (names) names[w] = kSlotNames[i];
+    if (total_ms) total_ms[w] = ms[i];
+    if (launches) launches[w] = cnt[i];
+    ++w;
+  }
+  return w;
 }
 
 }  // extern "C"

@@ -36,7 +36,7 @@ FOVEA_MAX_KMAX = 1024
 EXPORTED = [
     "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
     "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
-    "fovea_last_error",
+    "fovea_last_error", "fovea_profile", "fovea_profile_read",
 ]
 
 
@@ -84,6 +84,11 @@ def _load() -> ctypes.CDLL:
         vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.fovea_last_error.restype = ctypes.c_int
     lib.fovea_last_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.fovea_profile.restype = ctypes.c_int
+    lib.fovea_profile.argtypes = [vp, i32]
+    lib.fovea_profile_read.restype = i32
+    lib.fovea_profile_read.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_char_p),
+                                       ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
     return lib
 
 
@@ -178,6 +183,21 @@ def fovea_last_error(ctx: int, stream=None) -> tuple[int, int]:
     bits = ctypes.c_uint32(0)
     st = lib.fovea_last_error(ctx, _stream(stream), ctypes.byref(bits))
     return st, bits.value
+
+
+def fovea_profile(ctx: int, enable: bool) -> None:
+    _check(lib.fovea_profile(ctx, 1 if enable else 0), "fovea_profile")
+
+
+def fovea_profile_read(ctx: int, max_kernels: int = 16) -> dict:
+    """{kernel name: (total milliseconds, launches)} recorded since the last read."""
+    names = (ctypes.c_char_p * max_kernels)()
+    ms = (ctypes.c_float * max_kernels)()
+    cnt = (ctypes.c_int32 * max_kernels)()
+    n = lib.fovea_profile_read(ctx, max_kernels, names, ms, cnt)
+    if n < 0:
+        raise FoveaError(FOVEA_ERR_DEVICE, "fovea_profile_read")
+    return {names[i].decode(): (ms[i], cnt[i]) for i in range(n)}
 
 
 # ------------------------------------------------------------------------------------

@@ -28,7 +28,7 @@ def test_header_declares_the_entry_points():
     assert _declared() == sorted([
         "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
         "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
-        "fovea_last_error"])
+        "fovea_last_error", "fovea_profile", "fovea_profile_read"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -93,4 +93,6 @@ def test_null_context_paths(lib):
     assert st == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_build_memory(None, 1, None, None, None, None) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_last_error(None, None, None) == lib.FOVEA_ERR_INVALID_ARG
+    assert lib.lib.fovea_profile(None, 1) == lib.FOVEA_ERR_INVALID_ARG
+    assert lib.lib.fovea_profile_read(None, 4, None, None, None) == -1
     lib.lib.fovea_destroy(None)
