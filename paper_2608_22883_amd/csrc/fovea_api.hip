@@ -226,6 +226,47 @@ struct RFArgs {
   char* ws;
 };
 
+// Keys per score block: 64, 80 or 96, whichever spreads B * tiles blocks over the 256
+// compute units in the fewest waves of work per unit (cost = rounds x keys per block).
+int score_keys_per_block(int B, int m_max) {
+  int best = 4;
+  long best_cost = -1;
+  for (int kb = 4; kb <= 6; ++kb) {
+    const long blocks = static_cast<long>(B) * ((m_max + 16 * kb - 1) / (16 * kb));
+    const long cost = ((blocks + 255) / 256) * kb;
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best = kb;
+    }
+  }
+  return 16 * best;
+}
+
+typedef void (*ScoreKernel)(int, const int64_t*, int64_t, int, const int32_t*, int, int,
+                            const bf16_t*, int, const bf16_t*, float, float*);
+
+template <int NKC>
+ScoreKernel score_kernel_kb(int kb) {
+  switch (kb) {
+    case 5: return score_bf16_kernel<NKC, 5>;
+    case 6: return score_bf16_kernel<NKC, 6>;
+    default: return score_bf16_kernel<NKC, 4>;
+  }
+}
+
+ScoreKernel score_kernel_for(int nkc, int kb) {
+  switch (nkc) {
+    case 4: return score_kernel_kb<4>(kb);
+    case 8: return score_kernel_kb<8>(kb);
+    case 12: return score_kernel_kb<12>(kb);
+    case 14: return score_kernel_kb<14>(kb);
+    case 16: return score_kernel_kb<16>(kb);
+    case 20: return score_kernel_kb<20>(kb);
+    case 24: return score_kernel_kb<24>(kb);
+    default: return score_bf16_any_kernel;
+  }
+}
+
 template <typename T>
 fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   const fovea_dims& D = c->dims;
@@ -258,12 +299,23 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   }
   // 3. scores for every (node, key) of each request
   if (a.m_max > 0) {
-    const int tiles = (a.m_max + 63) / 64;
     const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.d_m)));
     ProfScope ps(c, kScore, s);
-    hipLaunchKernelGGL(score_kernel<T>, dim3(a.B * tiles), dim3(256), 0, s, a.B, a.mem_off,
-                       a.n_mem, a.m_max, a.node_off, a.n, a.t_max, static_cast<const T*>(a.keys),
-                       D.d_m, static_cast<const T*>(q), scale, S);
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      const int kb = score_keys_per_block(a.B, a.m_max) / 16;
+      const int tiles = (a.m_max + 16 * kb - 1) / (16 * kb);
+      auto kern = score_kernel_for(D.d_m / score_cfg::KC, kb);
+      const int grid = xcd_grid(a.B * (kern == score_bf16_any_kernel ? (a.m_max + 63) / 64 : tiles));
+      hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, a.B, a.mem_off, a.n_mem, a.m_max,
+                         a.node_off, a.n, a.t_max, static_cast<const bf16_t*>(a.keys), D.d_m,
+                         reinterpret_cast<const bf16_t*>(q), scale, S);
+    } else {
+      const int tiles = (a.m_max + 63) / 64;
+      hipLaunchKernelGGL(score_f32_kernel, dim3(xcd_grid(a.B * tiles)), dim3(256), 0, s, a.B,
+                         a.mem_off, a.n_mem, a.m_max, a.node_off, a.n, a.t_max,
+                         static_cast<const float*>(a.keys), D.d_m, reinterpret_cast<const float*>(q),
+                         scale, S);
+    }
   }
   // 4. selection and gather, one block per node
   SelectArgs<T> sa;
@@ -284,14 +336,33 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   sa.idx_out = a.idx_out;
   sa.mass_out = a.mass_out;
   sa.err = c->err;
-  const size_t sel_smem = static_cast<size_t>(a.m_max) * 4;
-  if (sel_smem > 0)
-    FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  static_cast<int>(sel_smem)));
   {
     ProfScope ps(c, kSelect, s);
-    hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
+    const bool wave_path = a.k_max <= kWaveSelKmax && a.m_max <= 64 * 64;
+    if (wave_path) {
+      const dim3 grid(xcd_grid((a.n + 3) / 4)), blk(256);
+      const int npl = (a.m_max + 63) / 64;
+#define FOVEA_SEL(N) hipLaunchKernelGGL((select_block_kernel<T, N>), grid, blk, 0, s, sa, a.n)
+      if (npl <= 1) FOVEA_SEL(1);
+      else if (npl <= 2) FOVEA_SEL(2);
+      else if (npl <= 4) FOVEA_SEL(4);
+      else if (npl <= 6) FOVEA_SEL(6);
+      else if (npl <= 9) FOVEA_SEL(9);
+      else if (npl <= 12) FOVEA_SEL(12);
+      else if (npl <= 16) FOVEA_SEL(16);
+      else if (npl <= 24) FOVEA_SEL(24);
+      else if (npl <= 32) FOVEA_SEL(32);
+      else if (npl <= 48) FOVEA_SEL(48);
+      else FOVEA_SEL(64);
+#undef FOVEA_SEL
+    } else {
+      const size_t sel_smem = static_cast<size_t>(a.m_max) * 4;
+      if (sel_smem > 0)
+        FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      static_cast<int>(sel_smem)));
+      hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
+    }
   }
   // 5. correction layer 1 (+ gate logit partials)
   {

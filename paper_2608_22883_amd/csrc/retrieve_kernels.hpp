@@ -13,7 +13,7 @@ namespace fovea {
 // Limits shared with the host code.
 constexpr int kMaxM = 16384;
 constexpr int kMaxKmax = 1024;
-constexpr int kQSplitBf16 = 3;  // q = hi + mid + lo in bf16 for the score MFMA
+constexpr int kQSplitBf16 = 2;  // q = hi + lo in bf16 for the score MFMA
 
 // Bounds check of request b's node and memory ranges against the host-side sizes.
 struct Extent {
@@ -102,8 +102,8 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
 // Query projection with the LayerNorm folded into the epilogue:
 //   q = W_Q (LN(h) + E_dep[l]) = rstd * (W' h - mu * W' 1) + W_Q (b + E_dep[l]),
 // W' = W_Q diag(gain) packed at context creation, c1 = W' 1, c2[l] = W_Q (b + E_dep[l]).
-// bf16 storage writes q as three bf16 planes hi + mid + lo (exact split of the fp32
-// value) for the score MFMA; fp32 storage writes q itself.
+// bf16 storage writes q as two bf16 planes, hi = bf16(q) and lo = bf16(q - hi), for the
+// score MFMA (|q - hi - lo| <= 2^-16 |q|); fp32 storage writes q itself.
 // ---------------------------------------------------------------------------------
 
 template <typename T>
@@ -143,12 +143,8 @@ __global__ __launch_bounds__(256) void q_proj_kernel(int n, const T* __restrict_
         const int64_t o = static_cast<int64_t>(row) * d_m + col;
         if constexpr (std::is_same<T, bf16_t>::value) {
           const bf16_t hi = f32_to_bf16_bits(val);
-          const float r1 = val - bf16_bits_to_f32(hi);
-          const bf16_t mid = f32_to_bf16_bits(r1);
-          const bf16_t lo = f32_to_bf16_bits(r1 - bf16_bits_to_f32(mid));
           q[o] = hi;
-          q[plane + o] = mid;
-          q[2 * plane + o] = lo;
+          q[plane + o] = f32_to_bf16_bits(val - bf16_bits_to_f32(hi));
         } else {
           q[o] = val;
         }
@@ -158,35 +154,253 @@ __global__ __launch_bounds__(256) void q_proj_kernel(int n, const T* __restrict_
 }
 
 // ---------------------------------------------------------------------------------
-// Scores s = q . k / sqrt(d_m) for every (node, key) of a request.  One block per
-// (request, 64-key tile); wave w owns keys [16 w, 16 w + 16) of the tile and loops over
-// the request's nodes in chunks of 64.  Keys stream straight from HBM into registers
-// (each lane reads 16 consecutive k of one key row: 32 B for bf16), the query chunk is
-// staged once per block in LDS.  The k order inside a 64-wide step is permuted the
-// same way for both operands: lane group g = lane / 16 feeds k = 16 g + 0..15.
+// Work-item mapping that keeps the blocks of one request on one XCD: blocks are
+// dispatched round-robin over the 8 XCDs (block i on XCD i % 8), so item
+// x * per_xcd + j is given to block 8 j + x.  Returns -1 for padding blocks.
 // ---------------------------------------------------------------------------------
 
-template <typename T>
-__global__ __launch_bounds__(256) void score_kernel(int B, const int64_t* __restrict__ mem_off,
-                                                    int64_t n_mem, int m_max,
-                                                    const int32_t* __restrict__ node_off,
-                                                    int n_nodes, int t_max,
-                                                    const T* __restrict__ keys, int d_m,
-                                                    const T* __restrict__ q, float scale,
-                                                    float* __restrict__ S) {
-  constexpr bool kBf16 = std::is_same<T, bf16_t>::value;
-  constexpr int NS = kBf16 ? kQSplitBf16 : 1;  // q planes
-  constexpr int VEC = Elem<T>::kPer16B;
-  constexpr int LDQ = 64 + VEC;
-  constexpr int CH_ROW = 64 / VEC;           // 16-byte chunks per 64-wide q row
-  constexpr int CH_TOTAL = NS * 64 * CH_ROW;
-  static_assert(CH_TOTAL % 256 == 0, "q staging does not split over the block");
-  __shared__ __align__(16) T qs[NS][64][LDQ];
+constexpr int kXcds = 8;
 
-  const int b = blockIdx.x % B;
-  const int tile = blockIdx.x / B;
+__device__ __forceinline__ int xcd_item(int total) {
+  const int per_xcd = (total + kXcds - 1) / kXcds;
+  const int item = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  return item < total ? item : -1;
+}
+
+inline int xcd_grid(int total) { return kXcds * ((total + kXcds - 1) / kXcds); }
+
+// ---------------------------------------------------------------------------------
+// Scores s = q . k / sqrt(d_m), bf16 storage.  One block per (request, tile of 16 KB
+// keys), four waves; wave w owns node block w (16 nodes) of the current 64-node chunk
+// and all keys of the tile (KB 16x16 MFMA accumulators).  The k dimension is walked in
+// 64-wide chunks:
+//   * keys: the block stages each chunk ([16 KB keys][64 k]) into one of two LDS slots;
+//     every thread keeps the next DK chunks in flight in registers, so HBM latency
+//     hides behind DK chunks of matrix work;
+//   * q: each wave reads its own 16 rows of the two bf16 planes (hi, lo) straight from
+//     L2 into A-fragment registers, DQ chunks ahead;
+//   * k order inside a chunk is permuted identically for both operands: lane group
+//     g = lane / 16 feeds k = 16 g + 0..7 to the first MFMA and 16 g + 8..15 to the
+//     second;
+//   * the KB accumulator chains are interleaved so consecutive MFMAs are independent.
+// The chunk count NKC is a template parameter: every loop unrolls and every load is
+// unconditional (rows past the request are clamped and dropped at the store), which
+// keeps the wait counters exact so the prefetch queue is never drained.
+// ---------------------------------------------------------------------------------
+
+namespace score_cfg {
+constexpr int KC = 64;    // k per chunk
+constexpr int LDK = KC + 8;
+constexpr int DK = 6;     // key prefetch depth (chunks)
+constexpr int DQ = 3;     // q prefetch depth (chunks)
+constexpr int NS = kQSplitBf16;
+template <int KB>
+struct Tile {
+  static constexpr int KT = 16 * KB;                    // keys per block
+  static constexpr int KCH = (KT * 8 + 255) / 256;      // 16-byte staging loads per thread
+  static constexpr int ROWS = KCH * 32;                 // LDS rows (padding rows unused)
+};
+}  // namespace score_cfg
+
+template <int NKC, int KB>
+__global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf16_kernel(
+    int B, const int64_t* __restrict__ mem_off, int64_t n_mem, int m_max,
+    const int32_t* __restrict__ node_off, int n_nodes, int t_max, const bf16_t* __restrict__ keys,
+    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S) {
+  using namespace score_cfg;
+  using TL = Tile<KB>;
+  __shared__ __align__(16) bf16_t ks[2][TL::ROWS][LDK];
+  const int tiles = (m_max + TL::KT - 1) / TL::KT;
+  const int item = xcd_item(B * tiles);
+  if (item < 0) return;
+  const int b = item / tiles;
+  const int tile = item % tiles;
   const Extent e = request_extent(b, mem_off, n_mem, m_max, node_off, n_nodes, t_max);
   if (!e.nodes_ok || !e.mem_ok) return;  // the select kernel reports and fills NaN
+  const int M = static_cast<int>(e.m1 - e.m0);
+  const int Tn = e.t1 - e.t0;
+  const int i0 = tile * TL::KT;
+  if (i0 >= M || Tn == 0) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
+  const int64_t plane = static_cast<int64_t>(n_nodes) * d_m;
+  const bf16_t* kg[TL::KCH];
+  u32x4* kd0[TL::KCH];
+  u32x4* kd1[TL::KCH];
+#pragma unroll
+  for (int u = 0; u < TL::KCH; ++u) {
+    const int qi = tid + 256 * u;               // 16-byte chunk of the [rows][64] tile
+    const int row = qi >> 3, kofs = (qi & 7) * 8;
+    kg[u] = keys + (e.m0 + min(i0 + row, M - 1)) * d_m + kofs;
+    kd0[u] = reinterpret_cast<u32x4*>(&ks[0][row][kofs]);
+    kd1[u] = reinterpret_cast<u32x4*>(&ks[1][row][kofs]);
+  }
+  const bf16_t* kb0 = &ks[0][lane & 15][16 * g];
+  const bf16_t* kb1 = &ks[1][lane & 15][16 * g];
+
+  for (int cn = 0; cn < Tn; cn += 64) {
+    const int qrow = e.t0 + min(cn + 16 * w + (lane & 15), Tn - 1);
+    const bf16_t* qg = q + static_cast<int64_t>(qrow) * d_m + 16 * g;
+    u32x4 kr[DK][TL::KCH];
+    u32x4 qr[DQ][NS][2];
+    f32x4 acc[KB];
+#pragma unroll
+    for (int i = 0; i < KB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < DK; ++c)
+      if (c < NKC)
+#pragma unroll
+        for (int u = 0; u < TL::KCH; ++u) kr[c][u] = *reinterpret_cast<const u32x4*>(kg[u] + c * KC);
+#pragma unroll
+    for (int c = 0; c < DQ; ++c)
+      if (c < NKC)
+#pragma unroll
+        for (int p = 0; p < NS; ++p) {
+          qr[c][p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + c * KC);
+          qr[c][p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + c * KC + 8);
+        }
+#pragma unroll
+    for (int u = 0; u < TL::KCH; ++u) *kd0[u] = kr[0][u];
+    if (DK < NKC)
+#pragma unroll
+      for (int u = 0; u < TL::KCH; ++u) kr[0][u] = *reinterpret_cast<const u32x4*>(kg[u] + DK * KC);
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < NKC; ++c) {
+      if (c + 1 < NKC) {
+#pragma unroll
+        for (int u = 0; u < TL::KCH; ++u) *(((c + 1) & 1) ? kd1[u] : kd0[u]) = kr[(c + 1) % DK][u];
+        if (c + 1 + DK < NKC)
+#pragma unroll
+          for (int u = 0; u < TL::KCH; ++u)
+            kr[(c + 1) % DK][u] = *reinterpret_cast<const u32x4*>(kg[u] + (c + 1 + DK) * KC);
+      }
+      const bf16_t* kb = (c & 1) ? kb1 : kb0;
+      bf16x8 bfr[KB][2];
+#pragma unroll
+      for (int kblk = 0; kblk < KB; ++kblk) {
+        bfr[kblk][0] = *reinterpret_cast<const bf16x8*>(kb + kblk * 16 * LDK);
+        bfr[kblk][1] = *reinterpret_cast<const bf16x8*>(kb + kblk * 16 * LDK + 8);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int p = 0; p < NS; ++p)
+#pragma unroll
+          for (int kblk = 0; kblk < KB; ++kblk)
+            acc[kblk] = mfma_bf16_16x16x32(*reinterpret_cast<const bf16x8*>(&qr[c % DQ][p][h]),
+                                           bfr[kblk][h], acc[kblk]);
+      if (c + DQ < NKC)
+#pragma unroll
+        for (int p = 0; p < NS; ++p) {
+          qr[c % DQ][p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c + DQ) * KC);
+          qr[c % DQ][p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c + DQ) * KC + 8);
+        }
+      __syncthreads();
+    }
+    if (cn + 16 * w < Tn) {
+#pragma unroll
+      for (int kblk = 0; kblk < KB; ++kblk) {
+        const int key = i0 + kblk * 16 + (lane & 15);
+        if (key >= M) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = cn + 16 * w + 4 * g + v;
+          if (r < Tn) S[static_cast<int64_t>(e.t0 + r) * m_max + key] = acc[kblk][v] * scale;
+        }
+      }
+    }
+  }
+}
+
+// Fallback for chunk counts without a fixed instantiation: same tiling (64 keys per
+// block), no register prefetch; each 64-k chunk is loaded, staged and consumed in turn.
+__global__ __launch_bounds__(256) void score_bf16_any_kernel(
+    int B, const int64_t* __restrict__ mem_off, int64_t n_mem, int m_max,
+    const int32_t* __restrict__ node_off, int n_nodes, int t_max, const bf16_t* __restrict__ keys,
+    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S) {
+  using namespace score_cfg;
+  constexpr int KT = 64;
+  __shared__ __align__(16) bf16_t ks[KT][LDK];
+  const int tiles = (m_max + KT - 1) / KT;
+  const int item = xcd_item(B * tiles);
+  if (item < 0) return;
+  const int b = item / tiles;
+  const int tile = item % tiles;
+  const Extent e = request_extent(b, mem_off, n_mem, m_max, node_off, n_nodes, t_max);
+  if (!e.nodes_ok || !e.mem_ok) return;
+  const int M = static_cast<int>(e.m1 - e.m0);
+  const int Tn = e.t1 - e.t0;
+  const int i0 = tile * KT;
+  if (i0 >= M || Tn == 0) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
+  const int64_t plane = static_cast<int64_t>(n_nodes) * d_m;
+  const int srow = tid >> 2, sk = (tid & 3) * 16;
+  const bf16_t* kg = keys + (e.m0 + min(i0 + srow, M - 1)) * d_m + sk;
+  for (int cn = 0; cn < Tn; cn += 64) {
+    const int qrow = e.t0 + min(cn + 16 * w + (lane & 15), Tn - 1);
+    const bf16_t* qg = q + static_cast<int64_t>(qrow) * d_m + 16 * g;
+    f32x4 acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < d_m; k0 += KC) {
+      reinterpret_cast<u32x4*>(&ks[srow][sk])[0] = *reinterpret_cast<const u32x4*>(kg + k0);
+      reinterpret_cast<u32x4*>(&ks[srow][sk])[1] = *reinterpret_cast<const u32x4*>(kg + k0 + 8);
+      u32x4 qa[NS][2];
+#pragma unroll
+      for (int p = 0; p < NS; ++p) {
+        qa[p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + k0);
+        qa[p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + k0 + 8);
+      }
+      __syncthreads();
+      const bf16_t* kb = &ks[lane & 15][16 * g];
+#pragma unroll
+      for (int kblk = 0; kblk < 4; ++kblk)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int p = 0; p < NS; ++p)
+            acc[kblk] = mfma_bf16_16x16x32(*reinterpret_cast<const bf16x8*>(&qa[p][h]),
+                                           *reinterpret_cast<const bf16x8*>(kb + kblk * 16 * LDK + 8 * h),
+                                           acc[kblk]);
+      __syncthreads();
+    }
+    if (cn + 16 * w < Tn) {
+#pragma unroll
+      for (int kblk = 0; kblk < 4; ++kblk) {
+        const int key = i0 + kblk * 16 + (lane & 15);
+        if (key >= M) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = cn + 16 * w + 4 * g + v;
+          if (r < Tn) S[static_cast<int64_t>(e.t0 + r) * m_max + key] = acc[kblk][v] * scale;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// Scores for fp32 storage (a simple version: one block per (request, 64-key tile),
+// wave w owns keys [16 w, 16 w + 16), fp32 MFMA, q staged per 64-k chunk in LDS).
+// ---------------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void score_f32_kernel(int B, const int64_t* __restrict__ mem_off,
+                                                        int64_t n_mem, int m_max,
+                                                        const int32_t* __restrict__ node_off,
+                                                        int n_nodes, int t_max,
+                                                        const float* __restrict__ keys, int d_m,
+                                                        const float* __restrict__ q, float scale,
+                                                        float* __restrict__ S) {
+  constexpr int LDQ = 64 + 4;
+  __shared__ __align__(16) float qs[64][LDQ];
+  const int tiles = (m_max + 63) / 64;
+  const int item = xcd_item(B * tiles);
+  if (item < 0) return;
+  const int b = item / tiles;
+  const int tile = item % tiles;
+  const Extent e = request_extent(b, mem_off, n_mem, m_max, node_off, n_nodes, t_max);
+  if (!e.nodes_ok || !e.mem_ok) return;
   const int M = static_cast<int>(e.m1 - e.m0);
   const int Tn = e.t1 - e.t0;
   const int i0 = tile * 64;
@@ -194,8 +408,7 @@ __global__ __launch_bounds__(256) void score_kernel(int B, const int64_t* __rest
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
   const int key = i0 + wave * 16 + (lane & 15);
-  const T* krow = keys + (e.m0 + min(key, M - 1)) * d_m + 16 * g;
-  const int64_t plane = static_cast<int64_t>(n_nodes) * d_m;
+  const float* krow = keys + (e.m0 + min(key, M - 1)) * d_m + 16 * g;
 
   for (int c0 = 0; c0 < Tn; c0 += 64) {
     const int nblk = min(4, (Tn - c0 + 15) / 16);
@@ -203,41 +416,24 @@ __global__ __launch_bounds__(256) void score_kernel(int B, const int64_t* __rest
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < d_m; k0 += 64) {
-      // key fragment: 16 consecutive k of this lane's key row
-      u32x4 kr[16 / VEC];
+      float kf[16];
 #pragma unroll
-      for (int u = 0; u < 16 / VEC; ++u)
-        kr[u] = *reinterpret_cast<const u32x4*>(krow + k0 + u * VEC);
-      // stage q[c0 .. c0+63][k0 .. k0+63] for every plane
+      for (int u = 0; u < 16; ++u) kf[u] = krow[k0 + u];
 #pragma unroll
-      for (int j = 0; j < CH_TOTAL / 256; ++j) {
-        const int c = tid + 256 * j;
-        const int p = c / (64 * CH_ROW);
-        const int rr = (c / CH_ROW) % 64;
-        const int cc = c % CH_ROW;
+      for (int j = 0; j < 4; ++j) {
+        const int c = tid + 256 * j;  // 64 rows x 16 chunks of 4 floats
+        const int rr = c >> 4, cc = (c & 15) * 4;
         const int src = e.t0 + min(c0 + rr, Tn - 1);
-        *reinterpret_cast<u32x4*>(&qs[p][rr][cc * VEC]) = *reinterpret_cast<const u32x4*>(
-            q + p * plane + static_cast<int64_t>(src) * d_m + k0 + cc * VEC);
+        *reinterpret_cast<u32x4*>(&qs[rr][cc]) =
+            *reinterpret_cast<const u32x4*>(q + static_cast<int64_t>(src) * d_m + k0 + cc);
       }
       __syncthreads();
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
         if (nb >= nblk) break;
-        const T* qrow = &qs[0][nb * 16 + (lane & 15)][16 * g];
-        if constexpr (kBf16) {
-          const bf16x8 kb0 = *reinterpret_cast<const bf16x8*>(&kr[0]);
-          const bf16x8 kb1 = *reinterpret_cast<const bf16x8*>(&kr[1]);
+        const float* qrow = &qs[nb * 16 + (lane & 15)][16 * g];
 #pragma unroll
-          for (int p = 0; p < NS; ++p) {
-            const T* qp = qrow + p * 64 * LDQ;
-            acc[nb] = mfma_bf16_16x16x32(*reinterpret_cast<const bf16x8*>(qp), kb0, acc[nb]);
-            acc[nb] = mfma_bf16_16x16x32(*reinterpret_cast<const bf16x8*>(qp + 8), kb1, acc[nb]);
-          }
-        } else {
-          const float* kf = reinterpret_cast<const float*>(kr);
-#pragma unroll
-          for (int s = 0; s < 16; ++s) acc[nb] = mfma_f32_16x16x4(qrow[s], kf[s], acc[nb]);
-        }
+        for (int s2 = 0; s2 < 16; ++s2) acc[nb] = mfma_f32_16x16x4(qrow[s2], kf[s2], acc[nb]);
       }
       __syncthreads();
     }
@@ -589,6 +785,365 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   if (tid == 0) {
     if (a.k_out) a.k_out[n] = K;
     if (a.mass_out) a.mass_out[n] = static_cast<float>(mass);
+  }
+}
+
+
+// ---------------------------------------------------------------------------------
+// Per-node selection and gather for memories of at most 64 * NPL entries and
+// k_max <= 256, one 256-thread block per node.
+// Selection (wave 0 only, no block barriers): each lane holds NPL order keys (entry
+// lane + 64 j).  The k_max-th largest key is found bit by bit (32 steps of a wave-wide
+// ballot count); ties at it are cut by a second bit search over the entry index so the
+// lowest indices win.  Candidates are compacted with ballot prefix counts, sorted
+// descending by (key, -index) in registers (<= 64) or in LDS (<= 256), then prefix
+// masses in fp64, K and the renormalised weights.
+// Gather (all four waves): thread -> (16-byte column chunk, row group); 16 value rows
+// in flight per thread per batch; row groups are summed in a fixed order.
+// ---------------------------------------------------------------------------------
+
+constexpr int kWaveSelKmax = 256;
+constexpr int kGatherRows = 32;  // value rows in flight per thread
+
+template <typename T>
+__device__ __forceinline__ void write_invalid_node(const SelectArgs<T>& a, int n, int tid, int nt) {
+  const float qnan = __builtin_nanf("");
+  const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
+  for (int c = tid; c < a.d_m; c += nt) {
+    st_f32(a.rT, rbase + c, qnan);
+    if (a.r_out) a.r_out[rbase + c] = qnan;
+  }
+  if (a.idx_out)
+    for (int t = tid; t < a.k_max; t += nt) a.idx_out[static_cast<int64_t>(n) * a.k_max + t] = -1;
+  if (tid == 0) {
+    if (a.k_out) a.k_out[n] = 0;
+    if (a.mass_out) a.mass_out[n] = qnan;
+  }
+}
+
+__device__ __forceinline__ int ballot_count(bool p) { return __popcll(__ballot(p)); }
+
+__device__ __forceinline__ unsigned long long comp_key(uint32_t k, int i) {
+  return (static_cast<unsigned long long>(k) << 32) |
+         static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(i));
+}
+
+// Orders the LDS accesses of one wave (a wave's LDS operations execute in issue order;
+// this keeps the compiler from moving them across the point).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One gather batch of up to NR value rows (t0, t0 + ng, ...): NR unconditional 16-byte
+// loads (row indices clamped to the last one due), then the weighted sums of the rows
+// that are due.  Advances t0 and left.
+template <typename T, int NR>
+__device__ __forceinline__ void gather_batch(const T* vbase, int d_m, const int* ix, const float* al,
+                                             int& t0, int ng, int& left, int c,
+                                             float (&acc)[Elem<T>::kPer16B]) {
+  constexpr int VEC = Elem<T>::kPer16B;
+  const int nr = min(NR, left);
+  u32x4 raw[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int t = t0 + min(r, nr - 1) * ng;
+    raw[r] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(ix[t]) * d_m + c * VEC);
+  }
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const float wgt = r < nr ? al[t0 + min(r, nr - 1) * ng] : 0.f;
+    const T* v = reinterpret_cast<const T*>(&raw[r]);
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) {
+      const float f = fmaf(wgt, Elem<T>::to_f32(v[x]), acc[x]);
+      acc[x] = r < nr ? f : acc[x];
+    }
+  }
+  t0 += nr * ng;
+  left -= nr;
+}
+
+// Selection for one node by one wave (see the comment above); writes the selected
+// indices and renormalised weights to idx_o / alpha_o and returns K (-1 if the node's
+// request is invalid, in which case its outputs have been written as NaN).
+template <typename T, int NPL>
+__device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, int lane,
+                                               unsigned long long* cand, double* pre_s,
+                                               float* alpha_o, int* idx_o, int64_t* m0_o,
+                                               float* mass_o) {
+  const int b = a.node_req[n];
+  int64_t m0 = 0, m1 = 0;
+  bool ok = b >= 0;
+  if (ok) {
+    m0 = a.mem_off[b];
+    m1 = a.mem_off[b + 1];
+    if (!(0 <= m0 && m0 <= m1 && m1 <= a.n_mem && m1 - m0 <= a.m_max)) {
+      ok = false;
+      if (lane == 0) atomicOr(a.err, kErrMemOff);
+    }
+  }
+  if (!ok) {
+    write_invalid_node(a, n, lane, 64);
+    return -1;
+  }
+  *m0_o = m0;
+  const int M = static_cast<int>(m1 - m0);
+  const float* srow = a.S + static_cast<int64_t>(n) * a.m_max;
+  uint32_t kv[NPL];
+  uint32_t kmax = 0;
+  int nV = 0;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int i = lane + 64 * j;
+    const bool v = i < M && (a.valid == nullptr || a.valid[m0 + i] != 0);
+    kv[j] = v ? order_key(srow[i]) : 0u;
+    kmax = max(kmax, kv[j]);
+    nV += ballot_count(v);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1)
+    kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), o, kWave)));
+  int K = 0;
+  double mass = 0.0;
+  if (nV > 0) {
+    const float smax = key_to_float(kmax);
+    double z = 0.0;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j)
+      if (kv[j] != 0u) z += static_cast<double>(expf(key_to_float(kv[j]) - smax));
+    const double Z = wave_sum(z);
+    const int C = min(nV, a.k_max);
+    uint32_t thr = 0u;
+    int ithr = 0x7FFFFFFF;
+    if (nV > a.k_max) {
+      // the k_max-th largest key, bit by bit (masked entries hold 0 and never count)
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t t = thr | (1u << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) cnt += ballot_count(kv[j] >= t);
+        if (cnt >= a.k_max) thr = t;
+      }
+      int gt = 0, eq = 0;
+#pragma unroll
+      for (int j = 0; j < NPL; ++j) {
+        gt += ballot_count(kv[j] > thr);
+        eq += ballot_count(kv[j] == thr);
+      }
+      const int need = a.k_max - gt;
+      if (eq > need) {
+        // largest I with #(tied, index < I) < need: the tied entries with index <= I stay
+        int I = 0;
+        for (int bit = 14; bit >= 0; --bit) {
+          const int t = I + (1 << bit);
+          int f = 0;
+#pragma unroll
+          for (int j = 0; j < NPL; ++j) f += ballot_count(kv[j] == thr && lane + 64 * j < t);
+          if (f < need) I = t;
+        }
+        ithr = I;
+      }
+    }
+    // compact the C candidates
+    int base = 0;
+    const unsigned long long lt = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const int i = lane + 64 * j;
+      const bool sel = kv[j] != 0u && (nV <= a.k_max || kv[j] > thr || (kv[j] == thr && i <= ithr));
+      const unsigned long long m = __ballot(sel);
+      const int pos = base + __popcll(m & lt);
+      if (sel && pos < kWaveSelKmax) cand[pos] = comp_key(kv[j], i);
+      base += __popcll(m);
+    }
+    const int Cc = min(C, base);
+    wave_lds_sync();
+    if (C <= 64) {
+      // sort in registers: lane t ends with rank t
+      unsigned long long x = lane < Cc ? cand[lane] : 0ull;
+#pragma unroll
+      for (int k2 = 2; k2 <= 64; k2 <<= 1) {
+#pragma unroll
+        for (int j2 = k2 >> 1; j2 > 0; j2 >>= 1) {
+          const unsigned long long y = static_cast<unsigned long long>(
+              __shfl_xor(static_cast<long long>(x), j2, kWave));
+          const bool lower = (lane & j2) == 0;
+          const bool desc = (lane & k2) == 0;
+          x = (lower == desc) ? (x > y ? x : y) : (x < y ? x : y);
+        }
+      }
+      const double e = lane < C ? static_cast<double>(expf(key_to_float(static_cast<uint32_t>(x >> 32)) - smax)) : 0.0;
+      double incl = e;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      wave_lds_sync();
+      cand[lane] = x;
+      pre_s[lane] = incl;
+    } else {
+      int P = 128;
+      while (P < C) P <<= 1;
+      for (int i = Cc + lane; i < P; i += 64) cand[i] = 0ull;
+      wave_lds_sync();
+      for (int k2 = 2; k2 <= P; k2 <<= 1) {
+        for (int j2 = k2 >> 1; j2 > 0; j2 >>= 1) {
+          for (int i = lane; i < P; i += 64) {
+            const int ixj = i ^ j2;
+            if (ixj > i) {
+              const unsigned long long x = cand[i], y = cand[ixj];
+              const bool desc = (i & k2) == 0;
+              if (desc ? (x < y) : (x > y)) {
+                cand[i] = y;
+                cand[ixj] = x;
+              }
+            }
+          }
+          wave_lds_sync();
+        }
+      }
+      double e4[4], loc = 0.0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int t = 4 * lane + u;
+        e4[u] = t < C ? static_cast<double>(expf(key_to_float(static_cast<uint32_t>(cand[t] >> 32)) - smax)) : 0.0;
+        loc += e4[u];
+        e4[u] = loc;
+      }
+      double incl = loc;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      const double off = incl - loc;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) pre_s[4 * lane + u] = off + e4[u];
+    }
+    wave_lds_sync();
+    // first rank whose prefix mass reaches tau
+    const double tau = static_cast<double>(a.tau[b]);
+    int first = 0x7FFFFFFF;
+    for (int t = lane; t < C; t += 64)
+      if (pre_s[t] / Z >= tau) first = min(first, t);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, kWave));
+    const int K_raw = first != 0x7FFFFFFF ? first + 1 : (C == nV ? nV : a.k_max + 1);
+    K = min(nV, min(a.k_max, max(a.k_min, K_raw)));
+    const double sumI = pre_s[K - 1];
+    mass = sumI / Z;
+    for (int t = lane; t < K; t += 64) {
+      const unsigned long long x = cand[t];
+      const float et = expf(key_to_float(static_cast<uint32_t>(x >> 32)) - smax);
+      alpha_o[t] = static_cast<float>(static_cast<double>(et) / sumI);
+      idx_o[t] = static_cast<int>(min(0xFFFFFFFFu - static_cast<uint32_t>(x), static_cast<uint32_t>(M - 1)));
+    }
+  }
+  *mass_o = static_cast<float>(mass);
+  return K;
+}
+
+template <typename T, int NPL>
+__global__ __launch_bounds__(256) void select_block_kernel(SelectArgs<T> a, int n_nodes) {
+  constexpr int VEC = Elem<T>::kPer16B;
+  constexpr int NW = 4;  // nodes per block, one selecting wave each
+  __shared__ unsigned long long cand[NW][kWaveSelKmax];
+  __shared__ double pre_s[NW][kWaveSelKmax];
+  __shared__ float alpha_s[NW][kWaveSelKmax];
+  __shared__ int idx_s[NW][kWaveSelKmax];
+  __shared__ __align__(16) float red[256 * VEC];
+  __shared__ int s_K[NW];
+  __shared__ int64_t s_m0[NW];
+  __shared__ float s_mass[NW];
+
+  const int item = xcd_item((n_nodes + NW - 1) / NW);
+  if (item < 0) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  {
+    const int n = item * NW + wave;
+    int K = -1;
+    int64_t m0 = 0;
+    float mass = 0.f;
+    if (n < n_nodes)
+      K = select_one_node<T, NPL>(a, n, lane, cand[wave], pre_s[wave], alpha_s[wave], idx_s[wave],
+                                  &m0, &mass);
+    if (lane == 0) {
+      s_K[wave] = K;
+      s_m0[wave] = m0;
+      s_mass[wave] = mass;
+    }
+  }
+  __syncthreads();
+
+  // ---- gather r = sum_t alpha_t u_{idx_t}, node by node: thread -> (chunk, row group) ----
+  const int cpr = a.d_m / VEC;                  // 16-byte chunks per value row
+  const int ng = cpr >= 256 ? 1 : 256 / cpr;    // row groups
+  for (int sn = 0; sn < NW; ++sn) {
+    const int n = item * NW + sn;
+    const int K = s_K[sn];
+    if (n >= n_nodes || K < 0) continue;        // block-uniform
+    const T* vbase = a.values + s_m0[sn] * a.d_m;
+    const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
+    const float* al = alpha_s[sn];
+    const int* ix = idx_s[sn];
+    for (int cp = 0; cp < cpr; cp += 256) {
+      const int c = cp + (tid % (cpr >= 256 ? 256 : cpr));
+      const int rg = cpr >= 256 ? 0 : tid / cpr;
+      const bool live = rg < ng && c < cpr;
+      float acc[VEC];
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) acc[x] = 0.f;
+      if (live) {
+        // rows t = rg, rg + ng, ... below K; the batch size follows the row count so that
+        // every load is unconditional (indices clamped to the last row) and the batch
+        // is one memory round trip
+        int t0 = rg;
+        int left = (K - rg + ng - 1) / ng;
+        while (left > 0) {
+          if (left > 16)
+            gather_batch<T, 32>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
+          else if (left > 8)
+            gather_batch<T, 16>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
+          else if (left > 4)
+            gather_batch<T, 8>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
+          else
+            gather_batch<T, 4>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
+        }
+      }
+      if (ng > 1) {
+        if (live) {
+#pragma unroll
+          for (int x = 0; x < VEC; ++x) red[(rg * cpr + c) * VEC + x] = acc[x];
+        }
+        __syncthreads();
+        if (live && rg == 0) {
+          for (int g2 = 1; g2 < ng; ++g2)
+#pragma unroll
+            for (int x = 0; x < VEC; ++x) acc[x] += red[(g2 * cpr + c) * VEC + x];
+        }
+      }
+      if (live && rg == 0) {
+        T outv[VEC];
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) outv[x] = Elem<T>::from_f32(acc[x]);
+        *reinterpret_cast<u32x4*>(a.rT + rbase + c * VEC) = *reinterpret_cast<const u32x4*>(outv);
+        if (a.r_out) {
+#pragma unroll
+          for (int x = 0; x < VEC; ++x) a.r_out[rbase + c * VEC + x] = acc[x];
+        }
+      }
+      if (ng > 1) __syncthreads();
+    }
+    if (a.idx_out)
+      for (int tt = tid; tt < a.k_max; tt += 256)
+        a.idx_out[static_cast<int64_t>(n) * a.k_max + tt] = tt < K ? ix[tt] : -1;
+    if (tid == 0) {
+      if (a.k_out) a.k_out[n] = K;
+      if (a.mass_out) a.mass_out[n] = s_mass[sn];
+    }
   }
 }
 

@@ -246,3 +246,16 @@ def test_host_argument_errors(lib):
                                 inp["h"], inp["depth"], inp["tau"], 1, 16, inp["h"], workspace=ws)
     assert e.value.status == lib.FOVEA_ERR_INVALID_ARG
     fv.close()
+
+
+@pytest.mark.parametrize("B,M,d_m", [(32, 576, 1024), (40, 576, 1024), (3, 130, 384), (5, 700, 896)],
+                         ids=["80-key-blocks", "96-key-blocks", "fallback-d384", "64-key-blocks-d896"])
+def test_score_tilings(lib, B, M, d_m):
+    """Each score-kernel tiling (keys per block chosen from the grid size) and the
+    unpipelined fallback agree with the oracle."""
+    wl = WORKLOADS["llava_b1"].with_(B=B, M=M, d=512, d_m=d_m, T=5, tau=0.7, tau_hi=0.95,
+                                     key_scale=(40.0, 200.0))
+    case = make_case(wl, affine="random")
+    g, st, _ = _run(lib, case)
+    assert st == 0
+    compare(case, g, run_oracle(case), H_TOL["bf16"])
