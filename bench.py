@@ -62,12 +62,13 @@ def kernel_model(wl, case, union_rows, k_sum):
     n_mem = int(Ms.sum())
     k = {}
     k["row_stats"] = dict(bytes=n * d * es + n * 8, flops=3 * n * d)
-    k["q_proj"] = dict(bytes=n * d * es + d_m * d * es + n * d_m * 4, flops=2 * n * d * d_m)
+    k["hq"] = dict(bytes=n * d * es + (d_m + 2 * d_c) * d * es + n * d_m * 4 + n * 2 * d_c * 4,
+                   flops=2 * n * d * (d_m + 2 * d_c))
     k["score"] = dict(bytes=n_mem * d_m * es + n * d_m * 4 + pairs * 4, flops=2 * pairs * d_m)
     k["select_gather"] = dict(bytes=pairs * 4 + union_rows * d_m * es + n * d_m * es,
                               flops=2 * int(k_sum) * d_m)
-    k["corr1"] = dict(bytes=n * (d + d_m) * es + 2 * d_c * (d + d_m) * es + n * d_c * es,
-                      flops=2 * n * (d + d_m) * 2 * d_c)
+    k["corr1"] = dict(bytes=n * d_m * es + 2 * d_c * d_m * es + n * 2 * d_c * 4 + n * d_c * es,
+                      flops=2 * n * d_m * 2 * d_c)
     k["corr2"] = dict(bytes=n * d_c * es + d * d_c * es + 2 * n * d * es, flops=2 * n * d_c * d)
     k["rms"] = dict(bytes=2 * n * d * es, flops=3 * n * d)
     # the retrieval as one operation: every key, q, the selected value rows, r
@@ -185,7 +186,7 @@ def main():
         gbs = m["bytes"] / (avg_ms * 1e-3) / 1e9
         tfl = m["flops"] / (avg_ms * 1e-3) / 1e12
         peak_fl = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
-        mfma = name in ("q_proj", "corr1", "corr2")
+        mfma = name in ("hq", "corr1", "corr2")
         kernels.append(dict(
             name=name, avg_us=round(avg_ms * 1e3, 2), launches=cnt, alg_bytes=m["bytes"],
             alg_flops=m["flops"], GBs=round(gbs, 1), TFLOPs=round(tfl, 2),

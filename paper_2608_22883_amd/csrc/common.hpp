@@ -57,6 +57,37 @@ __device__ __forceinline__ void st_f32(T* p, int64_t i, float v) {
   p[i] = Elem<T>::from_f32(v);
 }
 
+// 8 consecutive elements (16 bytes of bf16, 32 of fp32) to / from fp32; p 16-byte aligned.
+__device__ __forceinline__ void load8(const float* p, float (&x)[8]) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p);
+  const f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+  x[0] = a[0]; x[1] = a[1]; x[2] = a[2]; x[3] = a[3];
+  x[4] = b[0]; x[5] = b[1]; x[6] = b[2]; x[7] = b[3];
+}
+
+__device__ __forceinline__ void load8(const bf16_t* p, float (&x)[8]) {
+  const u32x4 a = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(a[e] << 16);
+    x[2 * e + 1] = __uint_as_float(a[e] & 0xffff0000u);
+  }
+}
+
+__device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{x[0], x[1], x[2], x[3]};
+  *reinterpret_cast<f32x4*>(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+}
+
+__device__ __forceinline__ void store8(bf16_t* p, const float (&x)[8]) {
+  u32x4 a;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    a[e] = static_cast<uint32_t>(f32_to_bf16_bits(x[2 * e])) |
+           (static_cast<uint32_t>(f32_to_bf16_bits(x[2 * e + 1])) << 16);
+  *reinterpret_cast<u32x4*>(p) = a;
+}
+
 // ---------------------------------------------------------------------------------
 // wave / block reductions (wave64)
 // ---------------------------------------------------------------------------------

@@ -8,130 +8,126 @@
 
 namespace fovea {
 
-constexpr int kCorrWM = 2, kCorrWN = 2, kCorrTM = 2, kCorrTN = 4;  // 64 x 128 block tile
-constexpr int kPartCols = kCorrTN * 16;  // columns reduced into one partial sum (one wave)
+template <typename T>
+using Corr1Cfg = GemmCfg<T, 64, 4>;
+template <typename T>
+using Corr2Cfg = GemmCfg<T, 128, 2>;
+template <typename T>
+using MemCfg = GemmCfg<T, 128, 4>;
+constexpr int kPartCols = 128;  // columns reduced into one partial sum (one block tile)
+
+__host__ __device__ constexpr int n_parts(int cols) { return (cols + kPartCols - 1) / kPartCols; }
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
 __device__ __forceinline__ float sigmoid_f(float x) { return 1.0f / (1.0f + expf(-x)); }
 
-// Layer 1 of both nets in one GEMM: [a_c | a_g] = SiLU([h ; r] [W_c1 ; W_g1]^T + [b_c1 ; b_g1]).
+// Layer 1 of both nets: [a_c | a_g] = SiLU(P + r W1r^T + [b_c1 ; b_g1]), where P = h W1h^T
+// comes from the hidden-state GEMM, so only the r half (K = d_m) is computed here.
 // a_c (correction hidden) is stored in the storage dtype for layer 2; the gate hidden
-// a_g is consumed here: each wave reduces SiLU(.) * w_g2 over its 64 columns into one
-// partial of the gate logit per row (gate_part[row][slot], deterministic order).
+// a_g is consumed here: each block reduces SiLU(.) * w_g2 over its 128 columns into one
+// partial of the gate logit per row (gate_part[row][tile column], deterministic order;
+// tiles without gate columns write 0).
 template <typename T>
-__global__ __launch_bounds__(256) void corr1_kernel(int n, const T* __restrict__ h, int d,
-                                                    const T* __restrict__ rT, int d_m,
-                                                    const T* __restrict__ W1,
+__global__ __launch_bounds__(256) void corr1_kernel(TileMap tm, int n, const T* __restrict__ rT,
+                                                    int d_m, const T* __restrict__ W1r,
+                                                    const float* __restrict__ P,
                                                     const float* __restrict__ b1, int d_c,
                                                     const float* __restrict__ w_g2,
                                                     T* __restrict__ a_c,
                                                     float* __restrict__ gate_part) {
-  constexpr int WM = kCorrWM, WN = kCorrWN, TM = kCorrTM, TN = kCorrTN;
-  using C = GemmCfg<T, WM, WN, TM, TN>;
+  using C = Corr1Cfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
-  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
-  const int N = 2 * d_c, K = d + d_m;
-  f32x4 acc[TM][TN];
-  gemm_mainloop<T, WM, WN, TM, TN>(acc, AConcat<T>{h, d, rT, d_m, d}, n, W1, K, N, K, m0, n0,
-                                   reinterpret_cast<T*>(smem));
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int col_base = n0 + wn * TN * 16;
-  if (col_base >= N) return;
-  const int n_gp = d_c / kPartCols;
-  if (col_base < d_c) {
+  int tr, tc;
+  if (!tm.map(tr, tc)) return;
+  const int m0 = tr * C::BM, n0 = tc * C::BN;
+  const int N = 2 * d_c;
+  const int n_gp = n_parts(N);
+  f32x4 acc[C::TM][C::TN];
+  gemm_mainloop<C>(acc, rT, d_m, n, W1r, d_m, N, d_m, m0, n0, smem);
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8]) -> float {
+        if (row >= n || col0 >= N) return 0.f;
+        float p[8], b[8], pre[8];
+        load8(P + static_cast<int64_t>(row) * N + col0, p);
+        load8(b1 + col0, b);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = col_base + j * 16 + (lane & 15);
-      const float bias = b1[col];
+        for (int e = 0; e < 8; ++e) pre[e] = v[e] + p[e] + b[e];
+        if (col0 < d_c) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = m0 + wm * TM * 16 + i * 16 + 4 * (lane >> 4) + v;
-          if (row < n) st_f32(a_c, static_cast<int64_t>(row) * d_c + col, silu_f(acc[i][j][v] + bias));
+          for (int e = 0; e < 8; ++e) pre[e] = silu_f(pre[e]);
+          store8(a_c + static_cast<int64_t>(row) * d_c + col0, pre);
+          return 0.f;
         }
-    }
-  } else {
-    float wg[TN], bias[TN];
+        float wg[8];
+        load8(w_g2 + (col0 - d_c), wg);
+        float acc_g = 0.f;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = col_base + j * 16 + (lane & 15);
-      bias[j] = b1[col];
-      wg[j] = w_g2[col - d_c];
-    }
-    const int slot = (col_base - d_c) / kPartCols;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        float s = 0.f;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) s = fmaf(silu_f(acc[i][j][v] + bias[j]), wg[j], s);
-        s = sum16(s);
-        const int row = m0 + wm * TM * 16 + i * 16 + 4 * (lane >> 4) + v;
-        if ((lane & 15) == 0 && row < n) gate_part[static_cast<int64_t>(row) * n_gp + slot] = s;
-      }
-  }
+        for (int e = 0; e < 8; ++e) acc_g = fmaf(silu_f(pre[e]), wg[e], acc_g);
+        return acc_g;
+      },
+      [&](int row, float sum) {
+        if (row < n) gate_part[static_cast<int64_t>(row) * n_gp + tc] = sum;
+      });
 }
 
 // Layer 2 and the gated residual: c = a_c W_c2^T + b_c2, g = sigmoid(sum(gate_part) + b_g2),
 // h' = h + g c.  Without RMSNorm h' is the output; with it, h' goes to h_out and each
-// wave writes the partial sum of h'^2 over its 64 columns (rms_part[row][slot]).
+// block writes the partial sum of h'^2 over its 128 columns (rms_part[row][tile column]).
 template <typename T>
-__global__ __launch_bounds__(256) void corr2_kernel(int n, const T* __restrict__ a_c, int d_c,
-                                                    const T* __restrict__ Wc2, int d,
+__global__ __launch_bounds__(256) void corr2_kernel(TileMap tm, int n, const T* __restrict__ a_c,
+                                                    int d_c, const T* __restrict__ Wc2, int d,
                                                     const float* __restrict__ b_c2,
                                                     const float* __restrict__ gate_part,
                                                     float b_g2, const T* __restrict__ h,
                                                     T* __restrict__ h_out,
                                                     float* __restrict__ gate_out,
                                                     float* __restrict__ rms_part, int has_rms) {
-  constexpr int WM = kCorrWM, WN = kCorrWN, TM = kCorrTM, TN = kCorrTN;
-  using C = GemmCfg<T, WM, WN, TM, TN>;
+  using C = Corr2Cfg<T>;
+  static_assert(C::SMEM_BYTES >= C::OUT_BYTES + C::BM * 4, "gate staging");
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
-  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
-  f32x4 acc[TM][TN];
-  gemm_mainloop<T, WM, WN, TM, TN>(acc, ASingle<T>{a_c, d_c}, n, Wc2, d_c, d, d_c, m0, n0,
-                                   reinterpret_cast<T*>(smem));
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int col_base = n0 + wn * TN * 16;
-  if (col_base >= d) return;
-  const int n_gp = d_c / kPartCols;
-  const int n_rp = d / kPartCols;
-  float bias[TN];
-#pragma unroll
-  for (int j = 0; j < TN; ++j) bias[j] = b_c2[col_base + j * 16 + (lane & 15)];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = m0 + wm * TM * 16 + i * 16 + 4 * (lane >> 4) + v;
-      const bool live = row < n;
-      float g = 0.f;
-      if (live) {
-        float s = 0.f;
-        for (int p = 0; p < n_gp; ++p) s += gate_part[static_cast<int64_t>(row) * n_gp + p];
-        g = sigmoid_f(s + b_g2);
-      }
-      float ss = 0.f;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = col_base + j * 16 + (lane & 15);
-        if (live) {
-          const int64_t o = static_cast<int64_t>(row) * d + col;
-          const float hp = fmaf(g, acc[i][j][v] + bias[j], ld_f32(h, o));
-          st_f32(h_out, o, hp);
-          ss = fmaf(hp, hp, ss);
-        }
-      }
-      if (has_rms) {
-        ss = sum16(ss);
-        if ((lane & 15) == 0 && live) rms_part[static_cast<int64_t>(row) * n_rp + col_base / kPartCols] = ss;
-      }
-      if (gate_out != nullptr && blockIdx.y == 0 && wn == 0 && (lane & 15) == 0 && live) gate_out[row] = g;
+  int tr, tc;
+  if (!tm.map(tr, tc)) return;
+  const int m0 = tr * C::BM, n0 = tc * C::BN;
+  const int n_gp = n_parts(2 * d_c);
+  const int n_rp = n_parts(d);
+  f32x4 acc[C::TM][C::TN];
+  gemm_mainloop<C>(acc, a_c, d_c, n, Wc2, d_c, d, d_c, m0, n0, smem);
+  // gate of each row of the tile, next to the epilogue's staging area
+  float* sg = reinterpret_cast<float*>(smem + C::OUT_BYTES);
+  if (threadIdx.x < C::BM) {
+    const int row = m0 + threadIdx.x;
+    float g = 0.f;
+    if (row < n) {
+      float sum = 0.f;
+      for (int p2 = 0; p2 < n_gp; ++p2) sum += gate_part[static_cast<int64_t>(row) * n_gp + p2];
+      g = sigmoid_f(sum + b_g2);
+      if (gate_out != nullptr && tc == 0) gate_out[row] = g;
     }
+    sg[threadIdx.x] = g;
+  }
+  // (the epilogue's first barrier orders these writes before any read)
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8]) -> float {
+        if (row >= n || col0 >= d) return 0.f;
+        const float g = sg[row - m0];
+        const int64_t o = static_cast<int64_t>(row) * d + col0;
+        float hv[8], b[8], hp[8];
+        load8(h + o, hv);
+        load8(b_c2 + col0, b);
+        float ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          hp[e] = fmaf(g, v[e] + b[e], hv[e]);
+          ss = fmaf(hp[e], hp[e], ss);
+        }
+        store8(h_out + o, hp);
+        return ss;
+      },
+      [&](int row, float sum) {
+        if (has_rms && row < n) rms_part[static_cast<int64_t>(row) * n_rp + tc] = sum;
+      });
 }
 
 // RMSNorm of h' in place: h_out = h' / sqrt(mean(h'^2) + eps) * w, one block per row.
@@ -143,11 +139,11 @@ __global__ __launch_bounds__(256) void rms_kernel(int n, int d, const float* __r
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   if (tid < 64) {
-    const int n_rp = d / kPartCols;
-    float s = 0.f;
-    for (int p = tid; p < n_rp; p += 64) s += rms_part[static_cast<int64_t>(row) * n_rp + p];
-    s = wave_sum(s);
-    if (tid == 0) s_rstd = 1.0f / sqrtf(s / static_cast<float>(d) + eps);
+    const int n_rp = n_parts(d);
+    float s2 = 0.f;
+    for (int p2 = tid; p2 < n_rp; p2 += 64) s2 += rms_part[static_cast<int64_t>(row) * n_rp + p2];
+    s2 = wave_sum(s2);
+    if (tid == 0) s_rstd = 1.0f / sqrtf(s2 / static_cast<float>(d) + eps);
   }
   __syncthreads();
   const float rstd = s_rstd;
@@ -158,40 +154,37 @@ __global__ __launch_bounds__(256) void rms_kernel(int n, int d, const float* __r
 // Memory build: [keys | values] = LN(V) [W_K ; W_U]^T with the LayerNorm folded into the
 // epilogue exactly as in the query projection (c1 = W' 1, c2 = W b).
 template <typename T>
-__global__ __launch_bounds__(256) void mem_proj_kernel(int n, const T* __restrict__ V, int d_v,
-                                                       const T* __restrict__ Wku, int d_m,
+__global__ __launch_bounds__(256) void mem_proj_kernel(TileMap tm, int n, const T* __restrict__ V,
+                                                       int d_v, const T* __restrict__ Wku, int d_m,
                                                        const float2* __restrict__ stats,
                                                        const float* __restrict__ c1,
                                                        const float* __restrict__ c2,
                                                        T* __restrict__ keys, T* __restrict__ values) {
-  constexpr int WM = kCorrWM, WN = kCorrWN, TM = kCorrTM, TN = kCorrTN;
-  using C = GemmCfg<T, WM, WN, TM, TN>;
+  using C = MemCfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
-  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
+  int tr, tc;
+  if (!tm.map(tr, tc)) return;
+  const int m0 = tr * C::BM, n0 = tc * C::BN;
   const int N = 2 * d_m;
-  f32x4 acc[TM][TN];
-  gemm_mainloop<T, WM, WN, TM, TN>(acc, ASingle<T>{V, d_v}, n, Wku, d_v, N, d_v, m0, n0,
-                                   reinterpret_cast<T*>(smem));
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  f32x4 acc[C::TM][C::TN];
+  gemm_mainloop<C>(acc, V, d_v, n, Wku, d_v, N, d_v, m0, n0, smem);
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8]) -> float {
+        if (row >= n || col0 >= N) return 0.f;
+        const float2 st = stats[row];
+        float a[8], b[8], val[8];
+        load8(c1 + col0, a);
+        load8(c2 + col0, b);
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = m0 + wm * TM * 16 + i * 16 + 4 * (lane >> 4) + v;
-      if (row >= n) continue;
-      const float2 st = stats[row];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn * TN * 16 + j * 16 + (lane & 15);
-        if (col >= N) continue;
-        const float val = st.y * (acc[i][j][v] - st.x * c1[col]) + c2[col];
-        if (col < d_m)
-          st_f32(keys, static_cast<int64_t>(row) * d_m + col, val);
+        for (int e = 0; e < 8; ++e) val[e] = st.y * (v[e] - st.x * a[e]) + b[e];
+        if (col0 < d_m)
+          store8(keys + static_cast<int64_t>(row) * d_m + col0, val);
         else
-          st_f32(values, static_cast<int64_t>(row) * d_m + (col - d_m), val);
-      }
-    }
+          store8(values + static_cast<int64_t>(row) * d_m + (col0 - d_m), val);
+        return 0.f;
+      },
+      NoRowSum{});
 }
 
 // ---------------------------------------------------------------------------------

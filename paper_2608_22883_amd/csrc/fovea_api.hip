@@ -20,13 +20,13 @@ struct fovea_ctx {
   bool bf16;
   size_t es;  // bytes per stored element
   void* block;  // one allocation holding every packed array below
-  void* W_Q;    // [d_m, d] W_Q diag(q_ln_g), storage dtype
   float* q_c1;  // [d_m] row sums of the folded W_Q
   float* q_c2;  // [n_depth, d_m] W_Q (q_ln_b + E_dep[l])
   void* W_KU;   // [2 d_m, d_v] [W_K ; W_U] diag(mem_ln_g)
   float* m_c1;  // [2 d_m]
   float* m_c2;  // [2 d_m] [W_K ; W_U] mem_ln_b
-  void* W1;     // [2 d_c, d + d_m] [W_c1 ; W_g1]
+  void* W_hq;   // [d_m + 2 d_c, d] [W_Q diag(q_ln_g) ; W_c1[:, :d] ; W_g1[:, :d]]
+  void* W1r;    // [2 d_c, d_m]    [W_c1[:, d:] ; W_g1[:, d:]]
   float* b1;    // [2 d_c]
   void* W_c2;   // [d, d_c]
   float* b_c2;  // [d]
@@ -62,7 +62,7 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 // Byte offsets of the retrieve_fuse workspace regions.
 struct WsLayout {
-  size_t node_req, stats, q, S, rT, a_c, gate_part, rms_part, total;
+  size_t node_req, stats, q, P, S, rT, a_c, gate_part, rms_part, total;
 };
 
 WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
@@ -72,11 +72,12 @@ WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
   L.node_req = o; o = align_up(o + n * 4);
   L.stats = o; o = align_up(o + n * 8);
   L.q = o; o = align_up(o + n * dm.d_m * (dm.dtype == FOVEA_BF16 ? 2 * kQSplitBf16 : 4));
+  L.P = o; o = align_up(o + n * 2 * dm.d_c * 4);
   L.S = o; o = align_up(o + n * m_max * 4);
   L.rT = o; o = align_up(o + n * dm.d_m * es);
   L.a_c = o; o = align_up(o + n * dm.d_c * es);
-  L.gate_part = o; o = align_up(o + n * (dm.d_c / kPartCols) * 4);
-  L.rms_part = o; o = align_up(o + n * (dm.d / kPartCols) * 4);
+  L.gate_part = o; o = align_up(o + n * n_parts(2 * dm.d_c) * 4);
+  L.rms_part = o; o = align_up(o + n * n_parts(dm.d) * 4);
   L.total = o;
   return L;
 }
@@ -101,8 +102,8 @@ bool dims_supported(const fovea_dims* d) {
     if ((call) != hipSuccess) return FOVEA_ERR_DEVICE;    \
   } while (0)
 
-enum KernelSlot { kRowStats, kQProj, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kNumSlots };
-const char* const kSlotNames[kNumSlots] = {"row_stats", "q_proj", "score", "select_gather",
+enum KernelSlot { kRowStats, kHq, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kNumSlots };
+const char* const kSlotNames[kNumSlots] = {"row_stats", "hq", "score", "select_gather",
                                            "corr1", "corr2", "rms", "mem_row_stats", "mem_proj"};
 
 hipEvent_t prof_event(fovea_ctx* c) {
@@ -144,14 +145,14 @@ fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
   auto T_ = [](const void* x) { return static_cast<const T*>(x); };
   // folded projections
   hipLaunchKernelGGL(fold_gain_kernel<T>, dim3(1024), dim3(256), 0, s, T_(p->W_Q), T_(p->q_ln_g),
-                     static_cast<int64_t>(d_m), d, static_cast<T*>(c->W_Q));
+                     static_cast<int64_t>(d_m), d, static_cast<T*>(c->W_hq));
   hipLaunchKernelGGL(fold_gain_kernel<T>, dim3(1024), dim3(256), 0, s, T_(p->W_K), T_(p->mem_ln_g),
                      static_cast<int64_t>(d_m), d_v, static_cast<T*>(c->W_KU));
   hipLaunchKernelGGL(fold_gain_kernel<T>, dim3(1024), dim3(256), 0, s, T_(p->W_U), T_(p->mem_ln_g),
                      static_cast<int64_t>(d_m), d_v, static_cast<T*>(c->W_KU) + static_cast<int64_t>(d_m) * d_v);
   // row sums of the folded weights and the bias / depth terms
   auto rows = [](int items) { return dim3((items + 3) / 4); };
-  hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m), dim3(256), 0, s, static_cast<const T*>(c->W_Q),
+  hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m), dim3(256), 0, s, static_cast<const T*>(c->W_hq),
                      d_m, d, static_cast<const T*>(nullptr), static_cast<const T*>(nullptr), 1, c->q_c1);
   hipLaunchKernelGGL(row_dot_kernel<T>, rows(d_m * D.n_depth), dim3(256), 0, s, T_(p->W_Q), d_m, d,
                      T_(p->q_ln_b), T_(p->E_dep), D.n_depth, c->q_c2);
@@ -163,10 +164,18 @@ fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
                      T_(p->mem_ln_b), static_cast<const T*>(nullptr), 1, c->m_c2 + d_m);
   // correction / gate nets
   const size_t es = sizeof(T);
-  const size_t w1_half = static_cast<size_t>(d_c) * (d + d_m) * es;
-  FOVEA_HIP(hipMemcpyAsync(c->W1, p->W_c1, w1_half, hipMemcpyDeviceToDevice, s));
-  FOVEA_HIP(hipMemcpyAsync(static_cast<char*>(c->W1) + w1_half, p->W_g1, w1_half,
-                           hipMemcpyDeviceToDevice, s));
+  // first layer of both nets split by input: the h half joins W_Q in the hidden-state
+  // GEMM, the r half is its own GEMM
+  const size_t src_pitch = static_cast<size_t>(d + d_m) * es;
+  char* hq_rows = static_cast<char*>(c->W_hq) + static_cast<size_t>(d_m) * d * es;
+  FOVEA_HIP(hipMemcpy2DAsync(hq_rows, d * es, p->W_c1, src_pitch, d * es, d_c, hipMemcpyDeviceToDevice, s));
+  FOVEA_HIP(hipMemcpy2DAsync(hq_rows + static_cast<size_t>(d_c) * d * es, d * es, p->W_g1, src_pitch,
+                             d * es, d_c, hipMemcpyDeviceToDevice, s));
+  FOVEA_HIP(hipMemcpy2DAsync(c->W1r, d_m * es, static_cast<const char*>(p->W_c1) + d * es, src_pitch,
+                             d_m * es, d_c, hipMemcpyDeviceToDevice, s));
+  FOVEA_HIP(hipMemcpy2DAsync(static_cast<char*>(c->W1r) + static_cast<size_t>(d_c) * d_m * es,
+                             d_m * es, static_cast<const char*>(p->W_g1) + d * es, src_pitch,
+                             d_m * es, d_c, hipMemcpyDeviceToDevice, s));
   FOVEA_HIP(hipMemcpyAsync(c->W_c2, p->W_c2, static_cast<size_t>(d) * d_c * es,
                            hipMemcpyDeviceToDevice, s));
   hipLaunchKernelGGL(to_f32_kernel<T>, dim3(8), dim3(256), 0, s, T_(p->b_c1), d_c, c->b1);
@@ -190,13 +199,15 @@ fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* val
                        0, 0, static_cast<const float*>(nullptr), static_cast<int32_t*>(nullptr),
                        c->err);
   }
-  using C = GemmCfg<T, kCorrWM, kCorrWN, kCorrTM, kCorrTN>;
-  const dim3 grid((n + C::BM - 1) / C::BM, (2 * D.d_m + C::BN - 1) / C::BN);
+  using C = MemCfg<T>;
+  const TileMap tm = make_tile_map((n + C::BM - 1) / C::BM, (2 * D.d_m + C::BN - 1) / C::BN,
+                                   static_cast<double>(n) * D.d_v, 2.0 * D.d_m * D.d_v);
   {
     ProfScope ps(c, kMemProj, s);
-    hipLaunchKernelGGL(mem_proj_kernel<T>, grid, dim3(C::NT), 0, s, n, static_cast<const T*>(V),
-                       D.d_v, static_cast<const T*>(c->W_KU), D.d_m, c->build_stats, c->m_c1,
-                       c->m_c2, static_cast<T*>(keys), static_cast<T*>(values));
+    hipLaunchKernelGGL(mem_proj_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, n,
+                       static_cast<const T*>(V), D.d_v, static_cast<const T*>(c->W_KU), D.d_m,
+                       c->build_stats, c->m_c1, c->m_c2, static_cast<T*>(keys),
+                       static_cast<T*>(values));
   }
   FOVEA_HIP(hipGetLastError());
   return FOVEA_OK;
@@ -274,14 +285,13 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   int32_t* node_req = reinterpret_cast<int32_t*>(a.ws + L.node_req);
   float2* stats = reinterpret_cast<float2*>(a.ws + L.stats);
   T* q = reinterpret_cast<T*>(a.ws + L.q);
+  float* P = reinterpret_cast<float*>(a.ws + L.P);
   float* S = reinterpret_cast<float*>(a.ws + L.S);
   T* rT = reinterpret_cast<T*>(a.ws + L.rT);
   T* a_c = reinterpret_cast<T*>(a.ws + L.a_c);
   float* gate_part = reinterpret_cast<float*>(a.ws + L.gate_part);
   float* rms_part = reinterpret_cast<float*>(a.ws + L.rms_part);
   const T* h = static_cast<const T*>(a.h);
-  using C = GemmCfg<T, kCorrWM, kCorrWN, kCorrTM, kCorrTN>;
-  const int row_blocks = (a.n + C::BM - 1) / C::BM;
 
   // 1. LayerNorm statistics of h, node -> request map, depth / tau / offset checks
   {
@@ -290,12 +300,16 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
                        D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
                        node_req, c->err);
   }
-  // 2. q = W_Q (LN(h) + E_dep[l])
+  // 2. everything that depends on h alone: q = W_Q (LN(h) + E_dep[l]) and P = h W1h^T
   {
-    ProfScope ps(c, kQProj, s);
-    hipLaunchKernelGGL(q_proj_kernel<T>, dim3(row_blocks, (D.d_m + C::BN - 1) / C::BN),
-                       dim3(C::NT), 0, s, a.n, h, D.d, static_cast<const T*>(c->W_Q), D.d_m,
-                       stats, a.depth, node_req, D.n_depth, c->q_c1, c->q_c2, q);
+    using C = HqCfg<T>;
+    const int N = D.d_m + 2 * D.d_c;
+    const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (N + C::BN - 1) / C::BN,
+                                     static_cast<double>(a.n) * D.d, static_cast<double>(N) * D.d);
+    ProfScope ps(c, kHq, s);
+    hipLaunchKernelGGL(hq_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, a.n, h, D.d,
+                       static_cast<const T*>(c->W_hq), D.d_m, 2 * D.d_c, stats, a.depth, node_req,
+                       D.n_depth, c->q_c1, c->q_c2, q, P);
   }
   // 3. scores for every (node, key) of each request
   if (a.m_max > 0) {
@@ -305,7 +319,9 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
       const int kb = score_keys_per_block(a.B, a.m_max) / 16;
       const int tiles = (a.m_max + 16 * kb - 1) / (16 * kb);
       auto kern = score_kernel_for(D.d_m / score_cfg::KC, kb);
-      const int grid = xcd_grid(a.B * (kern == score_bf16_any_kernel ? (a.m_max + 63) / 64 : tiles));
+      const int nch = (a.t_max + 63) / 64;
+      const int grid = xcd_grid(kern == score_bf16_any_kernel ? a.B * ((a.m_max + 63) / 64)
+                                                              : a.B * tiles * nch);
       hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, a.B, a.mem_off, a.n_mem, a.m_max,
                          a.node_off, a.n, a.t_max, static_cast<const bf16_t*>(a.keys), D.d_m,
                          reinterpret_cast<const bf16_t*>(q), scale, S);
@@ -364,20 +380,25 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
     }
   }
-  // 5. correction layer 1 (+ gate logit partials)
+  // 5. correction layer 1: the r half, plus P, bias and SiLU (+ gate logit partials)
   {
+    using C = Corr1Cfg<T>;
+    const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (2 * D.d_c + C::BN - 1) / C::BN,
+                                     static_cast<double>(a.n) * D.d_m, 2.0 * D.d_c * D.d_m);
     ProfScope ps(c, kCorr1, s);
-    hipLaunchKernelGGL(corr1_kernel<T>, dim3(row_blocks, (2 * D.d_c + C::BN - 1) / C::BN),
-                       dim3(C::NT), 0, s, a.n, h, D.d, rT, D.d_m, static_cast<const T*>(c->W1),
-                       c->b1, D.d_c, c->w_g2, a_c, gate_part);
+    hipLaunchKernelGGL(corr1_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, a.n, rT, D.d_m,
+                       static_cast<const T*>(c->W1r), P, c->b1, D.d_c, c->w_g2, a_c, gate_part);
   }
   // 6. correction layer 2, gate, residual (+ RMS partials)
   T* h_out = static_cast<T*>(a.h_out);
   {
+    using C = Corr2Cfg<T>;
+    const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (D.d + C::BN - 1) / C::BN,
+                                     static_cast<double>(a.n) * D.d_c, static_cast<double>(D.d) * D.d_c);
     ProfScope ps(c, kCorr2, s);
-    hipLaunchKernelGGL(corr2_kernel<T>, dim3(row_blocks, (D.d + C::BN - 1) / C::BN), dim3(C::NT),
-                       0, s, a.n, a_c, D.d_c, static_cast<const T*>(c->W_c2), D.d, c->b_c2,
-                       gate_part, c->b_g2, h, h_out, a.gate_out, rms_part, c->rms_w ? 1 : 0);
+    hipLaunchKernelGGL(corr2_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, a.n, a_c, D.d_c,
+                       static_cast<const T*>(c->W_c2), D.d, c->b_c2, gate_part, c->b_g2, h, h_out,
+                       a.gate_out, rms_part, c->rms_w ? 1 : 0);
   }
   // 7. RMSNorm
   if (c->rms_w) {
@@ -432,13 +453,13 @@ fovea_status fovea_create(fovea_ctx** out, const fovea_dims* dims, const fovea_p
   }
   const int64_t d = dims->d, d_v = dims->d_v, d_m = dims->d_m, d_c = dims->d_c, nd = dims->n_depth;
   size_t o = 0;
-  const size_t oWQ = o; o = align_up(o + d_m * d * c->es);
+  const size_t oWhq = o; o = align_up(o + (d_m + 2 * d_c) * d * c->es);
   const size_t oQc1 = o; o = align_up(o + d_m * 4);
   const size_t oQc2 = o; o = align_up(o + nd * d_m * 4);
   const size_t oWKU = o; o = align_up(o + 2 * d_m * d_v * c->es);
   const size_t oMc1 = o; o = align_up(o + 2 * d_m * 4);
   const size_t oMc2 = o; o = align_up(o + 2 * d_m * 4);
-  const size_t oW1 = o; o = align_up(o + 2 * d_c * (d + d_m) * c->es);
+  const size_t oW1r = o; o = align_up(o + 2 * d_c * d_m * c->es);
   const size_t oB1 = o; o = align_up(o + 2 * d_c * 4);
   const size_t oWc2 = o; o = align_up(o + d * d_c * c->es);
   const size_t oBc2 = o; o = align_up(o + d * 4);
@@ -450,13 +471,13 @@ fovea_status fovea_create(fovea_ctx** out, const fovea_dims* dims, const fovea_p
     return FOVEA_ERR_DEVICE;
   }
   char* base = static_cast<char*>(c->block);
-  c->W_Q = base + oWQ;
+  c->W_hq = base + oWhq;
   c->q_c1 = reinterpret_cast<float*>(base + oQc1);
   c->q_c2 = reinterpret_cast<float*>(base + oQc2);
   c->W_KU = base + oWKU;
   c->m_c1 = reinterpret_cast<float*>(base + oMc1);
   c->m_c2 = reinterpret_cast<float*>(base + oMc2);
-  c->W1 = base + oW1;
+  c->W1r = base + oW1r;
   c->b1 = reinterpret_cast<float*>(base + oB1);
   c->W_c2 = base + oWc2;
   c->b_c2 = reinterpret_cast<float*>(base + oBc2);

@@ -1,14 +1,30 @@
-// MFMA GEMM mainloop for gfx950: acc[m, n] = sum_k A[m, k] * B[n, k].
+// MFMA GEMM for gfx950: acc[m, n] = sum_k A[m, k] * B[n, k], with an LDS-staged epilogue.
 //
-// A is a row-major activation ([rows, K], K contiguous) reached through a source
-// functor, so that a concatenation such as [h ; r] is read in place.  B is a row-major
-// weight [N, K] (the nn.Linear layout).  Both operands are staged through LDS in
-// 16-byte chunks (8 bf16 or 4 fp32): a k-tile is 8 chunks wide, the next tile is
-// fetched into registers while the current one feeds the matrix cores.
+// A is a row-major activation [rows, K] (K contiguous); B is a row-major weight [N, K]
+// (the nn.Linear layout).  Block tile BM x 128 run by 2 x 2 wave64s; each wave owns a
+// TM x TN grid of 16x16 MFMA accumulators.  Rows past M and columns past N are clamped
+// on load; the epilogue hands them to the caller's functor, which drops them.
 //
-// Block tile BM x BN with BM = WM*TM*16, BN = WN*TN*16, run by WM*WN wave64s; each
-// wave owns a TM x TN grid of 16x16 MFMA accumulators.  Rows past M and columns past
-// N are clamped on load (the kernels' epilogues drop them on store).
+// bf16 mainloop: global -> LDS by direct-to-LDS loads (no register staging), NST LDS
+// stages, k-tile kt + NST - 1 in flight while the matrix cores work on tile kt, one
+// barrier per k-step.  A k-tile row is 64 bf16 = 128 B = 8 chunks of 16 B, stored with
+// chunk c of row r at slot c ^ ((r >> 1) & 7): the 16 rows read by one fragment load
+// then fall on distinct bank groups.  A direct-to-LDS load writes lane L's 16 bytes at
+// LDS base + 16 L, so the swizzle is applied by choosing which global chunk each lane
+// fetches.  The wait before each barrier counts this thread's outstanding loads
+// exactly (loads retire in issue order), so tiles further ahead stay in flight.
+//
+// fp32 mainloop: register-staged copy into a double-buffered, padded LDS tile
+// (MFMA 16x16x4 f32).
+//
+// Epilogue: the accumulators go through LDS (fp32, one wave-row of the tile per pass),
+// and each thread then owns 8 consecutive columns of a row, so stores and the loads of
+// epilogue operands are 16-byte, row-contiguous.  The 16 threads of a row are 16
+// consecutive lanes; a per-row value returned by the functor is summed over them.
+//
+// Tiles are mapped to XCDs (blocks are dispatched round-robin over the 8 XCDs): the
+// tile grid is cut into an xr x xc grid of regions and region x runs on XCD x, so the
+// blocks sharing an XCD's L2 share A rows and B columns.
 #pragma once
 
 #include <type_traits>
@@ -17,129 +33,312 @@
 
 namespace fovea {
 
-template <typename T, int WM, int WN, int TM, int TN>
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+template <typename T, int BM_, int NST_ = 4>
 struct GemmCfg {
+  static constexpr int BM = BM_, BN = 128, WM = 2, WN = 2;
   static constexpr int NT = WM * WN * kWave;
-  static constexpr int BM = WM * TM * 16;
-  static constexpr int BN = WN * TN * 16;
+  static constexpr int TM = BM / WM / 16;
+  static constexpr int TN = BN / WN / 16;
   static constexpr int VEC = Elem<T>::kPer16B;  // elements per 16-byte chunk
   static constexpr int BK = 8 * VEC;            // k-tile: 64 bf16 or 32 fp32
-  static constexpr int LDK = BK + VEC;          // LDS row pitch, padded by one chunk
+  static constexpr bool DMA = VEC == 8;         // bf16: direct-to-LDS pipeline
+  static constexpr int NST = DMA ? NST_ : 2;
+  // bf16 rows are 128 B (swizzled), fp32 rows padded by one chunk
+  static constexpr int LDK = DMA ? BK : BK + VEC;
+  static constexpr int STAGE_BYTES = (BM + BN) * LDK * static_cast<int>(sizeof(T));
+  // direct-to-LDS loads per wave per k-tile (one load moves 8 rows)
+  static constexpr int A_DMA = BM / 8 / 4;
+  static constexpr int B_DMA = BN / 8 / 4;
+  // fp32 register staging: 16-byte chunks per thread per k-tile
   static constexpr int A_CHUNKS = BM * 8 / NT;
   static constexpr int B_CHUNKS = BN * 8 / NT;
-  static constexpr int SMEM_BYTES = (BM + BN) * LDK * static_cast<int>(sizeof(T));
-  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0, "tile does not split over the threads");
+  // epilogue staging: one wave-row (TM * 16 rows) of fp32 with a 4-float pad
+  static constexpr int SROWS = TM * 16;
+  static constexpr int SLD = BN + 4;
+  static constexpr int OUT_BYTES = SROWS * SLD * 4;
+  static constexpr int PIPE_BYTES = NST * STAGE_BYTES;
+  static constexpr int SMEM_BYTES = PIPE_BYTES > OUT_BYTES ? PIPE_BYTES : OUT_BYTES;
+  static_assert(BM == 64 || BM == 128, "block rows");
+  static_assert(NST >= 2 && NST <= 5, "pipeline depth");
+  static_assert(SMEM_BYTES <= 160 * 1024, "LDS");
 };
 
-// A operand read from one row-major matrix.
-template <typename T>
-struct ASingle {
-  const T* p;
-  int64_t ld;
-  __device__ __forceinline__ const T* at(int row, int k) const { return p + row * ld + k; }
-};
-
-// A operand read from the concatenation [x0 | x1] of two row-major matrices along k;
-// k0 (the width of x0) is a multiple of the k-tile.
-template <typename T>
-struct AConcat {
-  const T* p0;
-  int64_t ld0;
-  const T* p1;
-  int64_t ld1;
-  int k0;
-  __device__ __forceinline__ const T* at(int row, int k) const {
-    return k < k0 ? p0 + row * ld0 + k : p1 + row * ld1 + (k - k0);
+// Position of a block's tile in the (row-block, column-block) grid; false for padding.
+struct TileMap {
+  int rb, cb;  // tiles along M and N
+  int xr, xc;  // XCD regions along M and N (xr * xc == 8)
+  __device__ __forceinline__ bool map(int& tr, int& tc) const {
+    const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int rr = (rb + xr - 1) / xr, rc = (cb + xc - 1) / xc;
+    const int lr = slot / rc, lc = slot % rc;
+    tr = (xcd / xc) * rr + lr;
+    tc = (xcd % xc) * rc + lc;
+    return lr < rr && tr < rb && tc < cb;
   }
 };
 
-template <typename T, int WM, int WN, int TM, int TN, class ASrc>
-__device__ __forceinline__ void gemm_mainloop(f32x4 (&acc)[TM][TN], const ASrc& a, int M,
-                                              const T* __restrict__ Bw, int64_t ldb, int N,
-                                              int K, int m0, int n0, T* smem) {
-  using C = GemmCfg<T, WM, WN, TM, TN>;
-  T* As = smem;
-  T* Bs = smem + C::BM * C::LDK;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / WN;
-  const int wn = wave % WN;
+inline TileMap make_tile_map(int rb, int cb, double a_bytes, double b_bytes) {
+  // region grid minimising the bytes pulled into the 8 L2s: xc copies of A, xr of B
+  TileMap m{rb, cb, 8, 1};
+  double best = -1.0;
+  for (int xr = 1; xr <= 8; xr *= 2) {
+    const int xc = 8 / xr;
+    const double cost = xc * a_bytes + xr * b_bytes;
+    if (best < 0.0 || cost < best) {
+      best = cost;
+      m.xr = xr;
+      m.xc = xc;
+    }
+  }
+  return m;
+}
 
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+inline int tile_grid(const TileMap& m) {
+  return 8 * ((m.rb + m.xr - 1) / m.xr) * ((m.cb + m.xc - 1) / m.xc);
+}
 
-  u32x4 ra[C::A_CHUNKS];
-  u32x4 rb[C::B_CHUNKS];
-  const T* Aw = As + (wm * TM * 16 + (lane & 15)) * C::LDK;
-  const T* Bwv = Bs + (wn * TN * 16 + (lane & 15)) * C::LDK;
-  const int nk = K / C::BK;
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits 3:0 and
+// 15:14, expcnt and lgkmcnt fields at their maxima, i.e. not waited on).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
-  for (int kt = 0; kt <= nk; ++kt) {
-    // fetch k-tile kt into registers (global -> VGPR)
-    if (kt < nk) {
-      const int k0 = kt * C::BK;
-#pragma unroll
-      for (int j = 0; j < C::A_CHUNKS; ++j) {
-        const int c = tid + j * C::NT;
-        const int row = min(m0 + (c >> 3), M - 1);
-        ra[j] = *reinterpret_cast<const u32x4*>(a.at(row, k0 + (c & 7) * C::VEC));
-      }
-#pragma unroll
-      for (int j = 0; j < C::B_CHUNKS; ++j) {
-        const int c = tid + j * C::NT;
-        const int row = min(n0 + (c >> 3), N - 1);
-        rb[j] = *reinterpret_cast<const u32x4*>(Bw + row * ldb + k0 + (c & 7) * C::VEC);
-      }
-    }
-    // consume k-tile kt - 1 from LDS while tile kt is in flight
-    if (kt > 0) {
-      if constexpr (std::is_same<T, bf16_t>::value) {
-#pragma unroll
-        for (int kk = 0; kk < C::BK; kk += 32) {
-          bf16x8 af[TM], bf[TN];
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-            af[i] = *reinterpret_cast<const bf16x8*>(Aw + i * 16 * C::LDK + kk + (lane >> 4) * 8);
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            bf[j] = *reinterpret_cast<const bf16x8*>(Bwv + j * 16 * C::LDK + kk + (lane >> 4) * 8);
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16_16x16x32(af[i], bf[j], acc[i][j]);
-        }
-      } else {
-#pragma unroll
-        for (int kk = 0; kk < C::BK; kk += 4) {
-          float af[TM], bf[TN];
-#pragma unroll
-          for (int i = 0; i < TM; ++i) af[i] = Aw[i * 16 * C::LDK + kk + (lane >> 4)];
-#pragma unroll
-          for (int j = 0; j < TN; ++j) bf[j] = Bwv[j * 16 * C::LDK + kk + (lane >> 4)];
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma_f32_16x16x4(af[i], bf[j], acc[i][j]);
-        }
-      }
-    }
-    if (kt == nk) break;
-    __syncthreads();  // everyone is done reading tile kt - 1
-#pragma unroll
-    for (int j = 0; j < C::A_CHUNKS; ++j) {
-      const int c = tid + j * C::NT;
-      *reinterpret_cast<u32x4*>(As + (c >> 3) * C::LDK + (c & 7) * C::VEC) = ra[j];
-    }
-#pragma unroll
-    for (int j = 0; j < C::B_CHUNKS; ++j) {
-      const int c = tid + j * C::NT;
-      *reinterpret_cast<u32x4*>(Bs + (c >> 3) * C::LDK + (c & 7) * C::VEC) = rb[j];
-    }
-    __syncthreads();  // tile kt is in LDS
+// Wait until at most `ahead` k-tiles of direct-to-LDS loads (NI loads each) are still
+// outstanding; ahead is clamped to MAXA (the pipeline's steady-state lead).
+template <int NI, int MAXA>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if constexpr (MAXA <= 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= MAXA)
+      wait_vmcnt<MAXA * NI>();
+    else
+      wait_tiles<NI, MAXA - 1>(ahead);
   }
 }
+
+// Workgroup barrier without a memory fence: a fence would also wait for the
+// direct-to-LDS loads still in flight.  The compiler barriers keep LDS accesses on
+// their side of it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <class C>
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[C::TM][C::TN]) {
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// bf16 mainloop (direct-to-LDS pipeline).  A: [M, K] row-major with leading dim lda.
+template <class C>
+__device__ __forceinline__ void gemm_mainloop_dma(f32x4 (&acc)[C::TM][C::TN],
+                                                  const bf16_t* __restrict__ A, int64_t lda, int M,
+                                                  const bf16_t* __restrict__ Bw, int64_t ldb, int N,
+                                                  int K, int m0, int n0, unsigned char* smem) {
+  constexpr int TM = C::TM, TN = C::TN, NST = C::NST;
+  constexpr int NI = C::A_DMA + C::B_DMA;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  zero_acc<C>(acc);
+
+  // sources and LDS row offsets of this thread's direct-to-LDS loads
+  const bf16_t* ga[C::A_DMA];
+  const bf16_t* gb[C::B_DMA];
+  int da[C::A_DMA], db[C::B_DMA];
+#pragma unroll
+  for (int j = 0; j < C::A_DMA; ++j) {
+    const int r0 = (wave * C::A_DMA + j) * 8;
+    const int row = r0 + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    ga[j] = A + static_cast<int64_t>(min(m0 + row, M - 1)) * lda + c * 8;
+    da[j] = r0 * 128;
+  }
+#pragma unroll
+  for (int j = 0; j < C::B_DMA; ++j) {
+    const int r0 = (wave * C::B_DMA + j) * 8;
+    const int row = r0 + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    gb[j] = Bw + static_cast<int64_t>(min(n0 + row, N - 1)) * ldb + c * 8;
+    db[j] = (C::BM + r0) * 128;
+  }
+  // fragment byte offsets (within a stage) for the two 32-wide k halves of a tile:
+  // lane reads chunk 4 h + lane / 16 of row (.. + lane % 16); the swizzle term is the
+  // same for all 16-row blocks of the lane
+  const int arow = wm * TM * 16 + (lane & 15);
+  const int brow = C::BM + wn * TN * 16 + (lane & 15);
+  int fa[2], fb[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    fa[h] = arow * 128 + (((4 * h + (lane >> 4)) ^ ((arow >> 1) & 7)) << 4);
+    fb[h] = brow * 128 + (((4 * h + (lane >> 4)) ^ ((brow >> 1) & 7)) << 4);
+  }
+
+  const int nk = K / C::BK;
+  auto issue = [&](int kt, int stage) {
+    unsigned char* st = smem + stage * C::STAGE_BYTES;
+    const int k0 = kt * C::BK;
+#pragma unroll
+    for (int j = 0; j < C::A_DMA; ++j)
+      __builtin_amdgcn_global_load_lds(ga[j] + k0, (lds_void_ptr)(st + da[j]), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < C::B_DMA; ++j)
+      __builtin_amdgcn_global_load_lds(gb[j] + k0, (lds_void_ptr)(st + db[j]), 16, 0, 0);
+  };
+
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_tiles<NI, NST - 2>(nk - 1 - kt);
+    lds_barrier();
+    if (kt + NST - 1 < nk) issue(kt + NST - 1, (kt + NST - 1) % NST);
+    const unsigned char* st = smem + (kt % NST) * C::STAGE_BYTES;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      bf16x8 af[TM], bf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8*>(st + fa[h] + i * 16 * 128);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bf[j] = *reinterpret_cast<const bf16x8*>(st + fb[h] + j * 16 * 128);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16_16x16x32(af[i], bf[j], acc[i][j]);
+    }
+  }
+  // every load has landed (none is issued past the last tile); LDS is free once all
+  // waves are done reading
+  lds_barrier();
+}
+
+// fp32 mainloop: register-staged, double-buffered LDS.
+template <class C>
+__device__ __forceinline__ void gemm_mainloop_f32(f32x4 (&acc)[C::TM][C::TN],
+                                                  const float* __restrict__ A, int64_t lda, int M,
+                                                  const float* __restrict__ Bw, int64_t ldb, int N,
+                                                  int K, int m0, int n0, unsigned char* smem_raw) {
+  constexpr int TM = C::TM, TN = C::TN;
+  float* smem = reinterpret_cast<float*>(smem_raw);
+  constexpr int STAGE = (C::BM + C::BN) * C::LDK;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  zero_acc<C>(acc);
+  const float* ga[C::A_CHUNKS];
+  const float* gb[C::B_CHUNKS];
+  int la[C::A_CHUNKS], lb[C::B_CHUNKS];
+#pragma unroll
+  for (int j = 0; j < C::A_CHUNKS; ++j) {
+    const int c = tid + j * C::NT;
+    ga[j] = A + static_cast<int64_t>(min(m0 + (c >> 3), M - 1)) * lda + (c & 7) * 4;
+    la[j] = (c >> 3) * C::LDK + (c & 7) * 4;
+  }
+#pragma unroll
+  for (int j = 0; j < C::B_CHUNKS; ++j) {
+    const int c = tid + j * C::NT;
+    gb[j] = Bw + static_cast<int64_t>(min(n0 + (c >> 3), N - 1)) * ldb + (c & 7) * 4;
+    lb[j] = (C::BM + (c >> 3)) * C::LDK + (c & 7) * 4;
+  }
+  const int aoff = (wm * TM * 16 + (lane & 15)) * C::LDK + (lane >> 4);
+  const int boff = (C::BM + wn * TN * 16 + (lane & 15)) * C::LDK + (lane >> 4);
+  const int nk = K / C::BK;
+  u32x4 ra[C::A_CHUNKS], rb[C::B_CHUNKS];
+#pragma unroll
+  for (int j = 0; j < C::A_CHUNKS; ++j) ra[j] = *reinterpret_cast<const u32x4*>(ga[j]);
+#pragma unroll
+  for (int j = 0; j < C::B_CHUNKS; ++j) rb[j] = *reinterpret_cast<const u32x4*>(gb[j]);
+  for (int kt = 0; kt < nk; ++kt) {
+    float* st = smem + (kt & 1) * STAGE;
+#pragma unroll
+    for (int j = 0; j < C::A_CHUNKS; ++j) *reinterpret_cast<u32x4*>(st + la[j]) = ra[j];
+#pragma unroll
+    for (int j = 0; j < C::B_CHUNKS; ++j) *reinterpret_cast<u32x4*>(st + lb[j]) = rb[j];
+    const int k1 = min(kt + 1, nk - 1) * C::BK;
+#pragma unroll
+    for (int j = 0; j < C::A_CHUNKS; ++j) ra[j] = *reinterpret_cast<const u32x4*>(ga[j] + k1);
+#pragma unroll
+    for (int j = 0; j < C::B_CHUNKS; ++j) rb[j] = *reinterpret_cast<const u32x4*>(gb[j] + k1);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < C::BK; kk += 4) {
+      float af[TM], bf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = st[aoff + i * 16 * C::LDK + kk];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bf[j] = st[boff + j * 16 * C::LDK + kk];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_f32_16x16x4(af[i], bf[j], acc[i][j]);
+    }
+  }
+  __syncthreads();
+}
+
+template <class C, typename T>
+__device__ __forceinline__ void gemm_mainloop(f32x4 (&acc)[C::TM][C::TN], const T* A, int64_t lda,
+                                              int M, const T* Bw, int64_t ldb, int N, int K, int m0,
+                                              int n0, unsigned char* smem) {
+  if constexpr (C::DMA)
+    gemm_mainloop_dma<C>(acc, A, lda, M, Bw, ldb, N, K, m0, n0, smem);
+  else
+    gemm_mainloop_f32<C>(acc, A, lda, M, Bw, ldb, N, K, m0, n0, smem);
+}
+
+// LDS-staged epilogue.  f(row, col0, v) sees the 8 accumulators of columns
+// col0 .. col0 + 7 of `row` (rows and columns past the matrix included: f drops them)
+// and returns a per-row contribution; fr(row, sum) receives the sum of the
+// contributions over the tile's 128 columns (lane order fixed, so deterministic).
+// Must be reached by every thread of the block.
+template <class C, class F, class FR>
+__device__ __forceinline__ void gemm_epilogue(const f32x4 (&acc)[C::TM][C::TN],
+                                              unsigned char* smem, int m0, int n0, F&& f,
+                                              FR&& fr) {
+  float* so = reinterpret_cast<float*>(smem);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  constexpr int GROUPS = C::SROWS * (C::BN / 8);
+  static_assert(GROUPS % C::NT == 0 && C::BN / 8 == 16, "epilogue mapping");
+#pragma unroll
+  for (int p = 0; p < C::WM; ++p) {
+    if (wm == p) {
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            so[(i * 16 + 4 * (lane >> 4) + v) * C::SLD + wn * C::TN * 16 + j * 16 + (lane & 15)] =
+                acc[i][j][v];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g0 = 0; g0 < GROUPS; g0 += C::NT) {
+      const int g = g0 + static_cast<int>(threadIdx.x);
+      const int r = g >> 4, c8 = g & 15;
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(so + r * C::SLD + c8 * 8);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(so + r * C::SLD + c8 * 8 + 4);
+      const float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      const int row = m0 + p * C::SROWS + r;
+      float s = f(row, n0 + c8 * 8, v);
+      s = sum16(s);
+      if ((lane & 15) == 0) fr(row, s);
+    }
+    __syncthreads();
+  }
+}
+
+struct NoRowSum {
+  __device__ __forceinline__ void operator()(int, float) const {}
+};
 
 }  // namespace fovea

@@ -107,50 +107,62 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
 // ---------------------------------------------------------------------------------
 
 template <typename T>
-__global__ __launch_bounds__(256) void q_proj_kernel(int n, const T* __restrict__ h, int d,
-                                                     const T* __restrict__ Wq, int d_m,
-                                                     const float2* __restrict__ stats,
-                                                     const int32_t* __restrict__ depth,
-                                                     const int32_t* __restrict__ node_req,
-                                                     int n_depth, const float* __restrict__ c1,
-                                                     const float* __restrict__ c2,
-                                                     T* __restrict__ q) {
-  constexpr int WM = 2, WN = 2, TM = 2, TN = 4;
-  using C = GemmCfg<T, WM, WN, TM, TN>;
+using HqCfg = GemmCfg<T, 128, 4>;
+
+// One GEMM over the hidden states for everything that depends on h alone:
+// columns [0, d_m) are the query projection (LayerNorm folded as described above),
+// columns [d_m, d_m + n_p) are h W1h^T, the h half of the correction and gate nets'
+// first layer, kept in fp32 for the layer-1 kernel (P, [n, n_p]).
+template <typename T>
+__global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __restrict__ h, int d,
+                                                 const T* __restrict__ Whq, int d_m, int n_p,
+                                                 const float2* __restrict__ stats,
+                                                 const int32_t* __restrict__ depth,
+                                                 const int32_t* __restrict__ node_req, int n_depth,
+                                                 const float* __restrict__ c1,
+                                                 const float* __restrict__ c2, T* __restrict__ q,
+                                                 float* __restrict__ P) {
+  using C = HqCfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
-  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
-  f32x4 acc[TM][TN];
-  gemm_mainloop<T, WM, WN, TM, TN>(acc, ASingle<T>{h, d}, n, Wq, d, d_m, d, m0, n0,
-                                   reinterpret_cast<T*>(smem));
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  int tr, tc;
+  if (!tm.map(tr, tc)) return;
+  const int m0 = tr * C::BM, n0 = tc * C::BN;
+  const int N = d_m + n_p;
+  f32x4 acc[C::TM][C::TN];
+  gemm_mainloop<C>(acc, h, d, n, Whq, d, N, d, m0, n0, smem);
   const int64_t plane = static_cast<int64_t>(n) * d_m;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = m0 + wm * TM * 16 + i * 16 + 4 * (lane >> 4) + v;
-      if (row >= n) continue;
-      const float2 st = stats[row];
-      const bool ok = node_req[row] >= 0;
-      const int dep = min(max(depth[row], 0), n_depth - 1);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn * TN * 16 + j * 16 + (lane & 15);
-        if (col >= d_m) continue;
-        float val = st.y * (acc[i][j][v] - st.x * c1[col]) + c2[dep * d_m + col];
-        if (!ok) val = __builtin_nanf("");
-        const int64_t o = static_cast<int64_t>(row) * d_m + col;
-        if constexpr (std::is_same<T, bf16_t>::value) {
-          const bf16_t hi = f32_to_bf16_bits(val);
-          q[o] = hi;
-          q[plane + o] = f32_to_bf16_bits(val - bf16_bits_to_f32(hi));
-        } else {
-          q[o] = val;
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8]) -> float {
+        if (row >= n || col0 >= N) return 0.f;
+        if (col0 >= d_m) {
+          store8(P + static_cast<int64_t>(row) * n_p + (col0 - d_m), v);
+          return 0.f;
         }
-      }
-    }
-  }
+        const float2 st = stats[row];
+        const bool ok = node_req[row] >= 0;
+        const int dep = min(max(depth[row], 0), n_depth - 1);
+        float a[8], b[8], val[8];
+        load8(c1 + col0, a);
+        load8(c2 + static_cast<int64_t>(dep) * d_m + col0, b);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) val[e] = ok ? st.y * (v[e] - st.x * a[e]) + b[e] : __builtin_nanf("");
+        const int64_t o = static_cast<int64_t>(row) * d_m + col0;
+        if constexpr (std::is_same<T, bf16_t>::value) {
+          float hi[8], lo[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            hi[e] = bf16_bits_to_f32(f32_to_bf16_bits(val[e]));
+            lo[e] = val[e] - hi[e];
+          }
+          store8(q + o, hi);
+          store8(q + plane + o, lo);
+        } else {
+          store8(q + o, val);
+        }
+        return 0.f;
+      },
+      NoRowSum{});
 }
 
 // ---------------------------------------------------------------------------------
@@ -171,14 +183,14 @@ inline int xcd_grid(int total) { return kXcds * ((total + kXcds - 1) / kXcds); }
 
 // ---------------------------------------------------------------------------------
 // Scores s = q . k / sqrt(d_m), bf16 storage.  One block per (request, tile of 16 KB
-// keys), four waves; wave w owns node block w (16 nodes) of the current 64-node chunk
-// and all keys of the tile (KB 16x16 MFMA accumulators).  The k dimension is walked in
+// keys, chunk of 64 nodes), four waves; wave w owns node block w (16 nodes) of the
+// chunk and all keys of the tile (KB 16x16 MFMA accumulators).  The k dimension is walked in
 // 64-wide chunks:
 //   * keys: the block stages each chunk ([16 KB keys][64 k]) into one of two LDS slots;
 //     every thread keeps the next DK chunks in flight in registers, so HBM latency
 //     hides behind DK chunks of matrix work;
 //   * q: each wave reads its own 16 rows of the two bf16 planes (hi, lo) straight from
-//     L2 into A-fragment registers, DQ chunks ahead;
+//     L2 into A-fragment registers, also DK chunks ahead;
 //   * k order inside a chunk is permuted identically for both operands: lane group
 //     g = lane / 16 feeds k = 16 g + 0..7 to the first MFMA and 16 g + 8..15 to the
 //     second;
@@ -192,7 +204,6 @@ namespace score_cfg {
 constexpr int KC = 64;    // k per chunk
 constexpr int LDK = KC + 8;
 constexpr int DK = 6;     // key prefetch depth (chunks)
-constexpr int DQ = 3;     // q prefetch depth (chunks)
 constexpr int NS = kQSplitBf16;
 template <int KB>
 struct Tile {
@@ -211,16 +222,18 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
   using TL = Tile<KB>;
   __shared__ __align__(16) bf16_t ks[2][TL::ROWS][LDK];
   const int tiles = (m_max + TL::KT - 1) / TL::KT;
-  const int item = xcd_item(B * tiles);
+  const int nch = (t_max + 63) / 64;  // 64-node chunks; a block takes one
+  const int item = xcd_item(B * tiles * nch);
   if (item < 0) return;
-  const int b = item / tiles;
-  const int tile = item % tiles;
+  const int b = item / (tiles * nch);
+  const int tile = (item / nch) % tiles;
+  const int cn = (item % nch) * 64;
   const Extent e = request_extent(b, mem_off, n_mem, m_max, node_off, n_nodes, t_max);
   if (!e.nodes_ok || !e.mem_ok) return;  // the select kernel reports and fills NaN
   const int M = static_cast<int>(e.m1 - e.m0);
   const int Tn = e.t1 - e.t0;
   const int i0 = tile * TL::KT;
-  if (i0 >= M || Tn == 0) return;
+  if (i0 >= M || cn >= Tn) return;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
   const int64_t plane = static_cast<int64_t>(n_nodes) * d_m;
@@ -238,32 +251,41 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
   const bf16_t* kb0 = &ks[0][lane & 15][16 * g];
   const bf16_t* kb1 = &ks[1][lane & 15][16 * g];
 
-  for (int cn = 0; cn < Tn; cn += 64) {
+  {
     const int qrow = e.t0 + min(cn + 16 * w + (lane & 15), Tn - 1);
     const bf16_t* qg = q + static_cast<int64_t>(qrow) * d_m + 16 * g;
     u32x4 kr[DK][TL::KCH];
-    u32x4 qr[DQ][NS][2];
+    u32x4 qr[DK][NS][2];
     f32x4 acc[KB];
 #pragma unroll
     for (int i = 0; i < KB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Loads retire in issue order (one counter for all vector memory), so they are
+    // issued in the order they are consumed: key chunk j + 1 is staged just before q
+    // chunk j is used, hence the issue order K0, K1, Q0, K2, Q1, ...  Scheduling
+    // barriers keep the compiler from hoisting later key loads above earlier q loads.
 #pragma unroll
-    for (int c = 0; c < DK; ++c)
-      if (c < NKC)
+    for (int u = 0; u < TL::KCH; ++u) kr[0][u] = *reinterpret_cast<const u32x4*>(kg[u]);
+#pragma unroll
+    for (int c = 1; c <= DK; ++c) {
+      if (c < DK && c < NKC)
 #pragma unroll
         for (int u = 0; u < TL::KCH; ++u) kr[c][u] = *reinterpret_cast<const u32x4*>(kg[u] + c * KC);
+      if (c == DK) {
+        // chunk 0 leaves its register slot for chunk DK
 #pragma unroll
-    for (int c = 0; c < DQ; ++c)
-      if (c < NKC)
+        for (int u = 0; u < TL::KCH; ++u) *kd0[u] = kr[0][u];
+        if (DK < NKC)
+#pragma unroll
+          for (int u = 0; u < TL::KCH; ++u) kr[0][u] = *reinterpret_cast<const u32x4*>(kg[u] + DK * KC);
+      }
+      if (c - 1 < NKC)
 #pragma unroll
         for (int p = 0; p < NS; ++p) {
-          qr[c][p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + c * KC);
-          qr[c][p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + c * KC + 8);
+          qr[c - 1][p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c - 1) * KC);
+          qr[c - 1][p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c - 1) * KC + 8);
         }
-#pragma unroll
-    for (int u = 0; u < TL::KCH; ++u) *kd0[u] = kr[0][u];
-    if (DK < NKC)
-#pragma unroll
-      for (int u = 0; u < TL::KCH; ++u) kr[0][u] = *reinterpret_cast<const u32x4*>(kg[u] + DK * KC);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     __syncthreads();
 #pragma unroll
     for (int c = 0; c < NKC; ++c) {
@@ -275,6 +297,7 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
           for (int u = 0; u < TL::KCH; ++u)
             kr[(c + 1) % DK][u] = *reinterpret_cast<const u32x4*>(kg[u] + (c + 1 + DK) * KC);
       }
+      __builtin_amdgcn_sched_barrier(0);
       const bf16_t* kb = (c & 1) ? kb1 : kb0;
       bf16x8 bfr[KB][2];
 #pragma unroll
@@ -288,13 +311,14 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
         for (int p = 0; p < NS; ++p)
 #pragma unroll
           for (int kblk = 0; kblk < KB; ++kblk)
-            acc[kblk] = mfma_bf16_16x16x32(*reinterpret_cast<const bf16x8*>(&qr[c % DQ][p][h]),
+            acc[kblk] = mfma_bf16_16x16x32(*reinterpret_cast<const bf16x8*>(&qr[c % DK][p][h]),
                                            bfr[kblk][h], acc[kblk]);
-      if (c + DQ < NKC)
+      __builtin_amdgcn_sched_barrier(0);
+      if (c + DK < NKC)
 #pragma unroll
         for (int p = 0; p < NS; ++p) {
-          qr[c % DQ][p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c + DQ) * KC);
-          qr[c % DQ][p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c + DQ) * KC + 8);
+          qr[c % DK][p][0] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c + DK) * KC);
+          qr[c % DK][p][1] = *reinterpret_cast<const u32x4*>(qg + p * plane + (c + DK) * KC + 8);
         }
       __syncthreads();
     }
