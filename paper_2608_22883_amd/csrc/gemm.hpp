@@ -193,31 +193,53 @@ __device__ __forceinline__ void gemm_mainloop_dma(f32x4 (&acc)[C::TM][C::TN],
     for (int j = 0; j < C::B_DMA; ++j)
       __builtin_amdgcn_global_load_lds(gb[j] + k0, (lds_void_ptr)(st + db[j]), 16, 0, 0);
   };
-
+  // Steady state of step kt: wait for tile kt (this thread's loads, then the barrier
+  // for everyone's), read its fragments, run its MFMAs, and load tile kt + NST - 1 into
+  // the stage that tile kt - 1 used.  Loads are issued for every step (past the last
+  // tile the last tile is loaded again into a stage nobody reads), so the number in
+  // flight is constant and the wait is a fixed count, and the body is one basic block
+  // in which the scheduling groups below interleave the LDS reads and the loads with
+  // the MFMAs: the first k half's reads go first, then the second half's reads and the
+  // loads each alternate with one MFMA.  Within a half the reads are ordered
+  // A0, B0..B(TN-1), A1.. as the i-major MFMAs first need them.
 #pragma unroll
-  for (int s = 0; s < NST - 1; ++s)
-    if (s < nk) issue(s, s);
-
+  for (int s = 0; s < NST - 1; ++s) issue(min(s, nk - 1), s);
   for (int kt = 0; kt < nk; ++kt) {
-    wait_tiles<NI, NST - 2>(nk - 1 - kt);
+    wait_vmcnt<(NST - 2) * NI>();
     lds_barrier();
-    if (kt + NST - 1 < nk) issue(kt + NST - 1, (kt + NST - 1) % NST);
     const unsigned char* st = smem + (kt % NST) * C::STAGE_BYTES;
+    bf16x8 af[2][TM], bf[2][TN];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      bf16x8 af[TM], bf[TN];
+      af[h][0] = *reinterpret_cast<const bf16x8*>(st + fa[h]);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8*>(st + fa[h] + i * 16 * 128);
+      for (int j = 0; j < TN; ++j) bf[h][j] = *reinterpret_cast<const bf16x8*>(st + fb[h] + j * 16 * 128);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bf[j] = *reinterpret_cast<const bf16x8*>(st + fb[h] + j * 16 * 128);
+      for (int i = 1; i < TM; ++i) af[h][i] = *reinterpret_cast<const bf16x8*>(st + fa[h] + i * 16 * 128);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16_16x16x32(af[i], bf[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16_16x16x32(af[h][i], bf[h][j], acc[i][j]);
+    issue(min(kt + NST - 1, nk - 1), (kt + NST - 1) % NST);
+    constexpr int NH = TM + TN;  // reads per k half
+    __builtin_amdgcn_sched_group_barrier(0x100, NH, 0);
+#pragma unroll
+    for (int t = 0; t < NH; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
+#pragma unroll
+    for (int t = 0; t < NI; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM * TN - NH - NI, 0);
   }
-  // every load has landed (none is issued past the last tile); LDS is free once all
-  // waves are done reading
+  // the extra loads of the last steps land before the LDS is reused
+  wait_vmcnt<0>();
   lds_barrier();
 }
 
