@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0    # dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3     # dense fp32
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_batched_b32.txt")
 
 
 def log(*a):
@@ -47,7 +48,52 @@ def parse():
     ap.add_argument("--copies", type=int, default=6, help="input copies rotated in the timed loop")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (counter calibration)")
     return ap.parse_args()
+
+
+def source_hash() -> str:
+    """Hash of the library sources; counter readings are valid for this hash only."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for sub in ("include", os.path.join("paper_2608_22883_amd", "csrc")):
+        base = os.path.join(ROOT, sub)
+        for name in sorted(os.listdir(base)):
+            with open(os.path.join(base, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary (FETCH_SIZE +
+    WRITE_SIZE, scaled by a plain copy's readings), or None when the summary is missing
+    or was taken on other sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rows = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+    except OSError:
+        return None
+    rows = {k.strip(): v.strip() for k, v in rows.items()}
+    if rows.get("source_hash") != source_hash():
+        return None
+    v = rows.get(f"traffic_bytes {kernel}")
+    return int(float(v)) if v else None
+
+
+def copy_calibration():
+    """A plain device-to-device copy of 256 MiB, ten times: the reference dispatch for
+    scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+
+    n = 256 << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps(dict(copy_bytes_read=n, copy_bytes_written=n, dispatches=10)), flush=True)
 
 
 def kernel_model(wl, case, union_rows, k_sum):
@@ -104,6 +150,9 @@ def cpu_baseline(case, budget_s):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the retrieval of each request is independent, "
@@ -198,10 +247,11 @@ def main():
     if dom["bound"] == "mfma":
         roof = dict(bound="mfma", achieved=dom["TFLOPs"],
                     peak=PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS,
-                    unit="TFLOP/s", frac=dom["frac"], traffic=None, kernel=dom["name"])
+                    unit="TFLOP/s", frac=dom["frac"], traffic=measured_traffic(dom["name"]),
+                    kernel=dom["name"])
     else:
         roof = dict(bound="hbm", achieved=dom["GBs"], peak=PEAK_HBM_GBS, unit="GB/s",
-                    frac=dom["frac"], traffic=None, kernel=dom["name"])
+                    frac=dom["frac"], traffic=measured_traffic(dom["name"]), kernel=dom["name"])
     ret_us = sum(k["avg_us"] for k in kernels if k["name"] in ("score", "select_gather"))
     ret_gbs = retrieval["bytes"] / (ret_us * 1e-6) / 1e9 if ret_us else 0.0
 
