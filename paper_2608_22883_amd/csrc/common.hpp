@@ -105,6 +105,75 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Wave-wide reductions on DPP and the gfx950 row swaps (VALU only, no LDS round trip):
+// xor 1 and xor 2 inside quads, half-row and row mirrors, then row pairs and wave
+// halves.  Every lane ends with the result; the combination order is fixed, so a
+// floating-point sum is deterministic.
+__device__ __forceinline__ uint32_t dpp_perm(uint32_t v, int sel) {
+  switch (sel) {
+    case 0: return __builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false);
+    case 1: return __builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false);
+    case 2: return __builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false);
+    default: return __builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false);
+  }
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int sel = 0; sel < 4; ++sel) v = max(v, dpp_perm(v, sel));
+  const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = max(static_cast<uint32_t>(p[0]), static_cast<uint32_t>(p[1]));
+  const auto q = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return max(static_cast<uint32_t>(q[0]), static_cast<uint32_t>(q[1]));
+}
+
+__device__ __forceinline__ int wave_sum_i32(int v) {
+#pragma unroll
+  for (int sel = 0; sel < 4; ++sel) v += static_cast<int>(dpp_perm(static_cast<uint32_t>(v), sel));
+  const auto p = __builtin_amdgcn_permlane16_swap(static_cast<uint32_t>(v), static_cast<uint32_t>(v), false, false);
+  v = static_cast<int>(p[0]) + static_cast<int>(p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(static_cast<uint32_t>(v), static_cast<uint32_t>(v), false, false);
+  return static_cast<int>(q[0]) + static_cast<int>(q[1]);
+}
+
+// Inclusive prefix sum over the 64 lanes (DPP row shifts, then row broadcasts).
+__device__ __forceinline__ int wave_incl_scan_i32(int v) {
+  const int x = v;
+  v += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, x, 0x113, 0xF, 0xF, false);  // row_shr:3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xE, false);  // row_shr:4, banks 1-3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xC, false);  // row_shr:8, banks 2-3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15, rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31, rows 2, 3
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int sel = 0; sel < 4; ++sel) {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const uint64_t lo = dpp_perm(static_cast<uint32_t>(u), sel);
+    const uint64_t hi = dpp_perm(static_cast<uint32_t>(u >> 32), sel);
+    v += __longlong_as_double(static_cast<long long>((hi << 32) | lo));
+  }
+  {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const auto pl = __builtin_amdgcn_permlane16_swap(static_cast<uint32_t>(u), static_cast<uint32_t>(u), false, false);
+    const auto ph = __builtin_amdgcn_permlane16_swap(static_cast<uint32_t>(u >> 32), static_cast<uint32_t>(u >> 32), false, false);
+    v = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(static_cast<uint32_t>(ph[0])) << 32) | static_cast<uint32_t>(pl[0]))) +
+        __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(static_cast<uint32_t>(ph[1])) << 32) | static_cast<uint32_t>(pl[1])));
+  }
+  {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const auto pl = __builtin_amdgcn_permlane32_swap(static_cast<uint32_t>(u), static_cast<uint32_t>(u), false, false);
+    const auto ph = __builtin_amdgcn_permlane32_swap(static_cast<uint32_t>(u >> 32), static_cast<uint32_t>(u >> 32), false, false);
+    v = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(static_cast<uint32_t>(ph[0])) << 32) | static_cast<uint32_t>(pl[0]))) +
+        __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(static_cast<uint32_t>(ph[1])) << 32) | static_cast<uint32_t>(pl[1])));
+  }
+  return v;
+}
+
 // Sum over the 16 lanes that share lane / 16 (one MFMA 16x16 output row group).
 __device__ __forceinline__ float sum16(float v) {
 #pragma unroll

@@ -354,23 +354,30 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   sa.err = c->err;
   {
     ProfScope ps(c, kSelect, s);
-    const bool wave_path = a.k_max <= kWaveSelKmax && a.m_max <= 64 * 64;
+    const int VEC = D.dtype == FOVEA_BF16 ? 8 : 4;
+    const int nch = (D.d_m / VEC + 63) / 64;  // 16-byte chunks per lane per value row
+    const bool wave_path = a.k_max <= kWaveSelKmax && a.m_max <= 64 * 64 && nch <= 4;
     if (wave_path) {
-      const dim3 grid(xcd_grid((a.n + 3) / 4)), blk(256);
+      const dim3 grid(xcd_grid((a.n + 1) / 2)), blk(256);
       const int npl = (a.m_max + 63) / 64;
-#define FOVEA_SEL(N) hipLaunchKernelGGL((select_block_kernel<T, N>), grid, blk, 0, s, sa, a.n)
-      if (npl <= 1) FOVEA_SEL(1);
-      else if (npl <= 2) FOVEA_SEL(2);
-      else if (npl <= 4) FOVEA_SEL(4);
-      else if (npl <= 6) FOVEA_SEL(6);
-      else if (npl <= 9) FOVEA_SEL(9);
-      else if (npl <= 12) FOVEA_SEL(12);
-      else if (npl <= 16) FOVEA_SEL(16);
-      else if (npl <= 24) FOVEA_SEL(24);
-      else if (npl <= 32) FOVEA_SEL(32);
-      else if (npl <= 48) FOVEA_SEL(48);
-      else FOVEA_SEL(64);
+#define FOVEA_SEL_C(N, C) hipLaunchKernelGGL((select_node_kernel<T, N, C>), grid, blk, 0, s, sa, a.n)
+#define FOVEA_SEL(N)              \
+  if (nch <= 1) FOVEA_SEL_C(N, 1); \
+  else if (nch <= 2) FOVEA_SEL_C(N, 2); \
+  else FOVEA_SEL_C(N, 4)
+      if (npl <= 1) { FOVEA_SEL(1); }
+      else if (npl <= 2) { FOVEA_SEL(2); }
+      else if (npl <= 4) { FOVEA_SEL(4); }
+      else if (npl <= 6) { FOVEA_SEL(6); }
+      else if (npl <= 9) { FOVEA_SEL(9); }
+      else if (npl <= 12) { FOVEA_SEL(12); }
+      else if (npl <= 16) { FOVEA_SEL(16); }
+      else if (npl <= 24) { FOVEA_SEL(24); }
+      else if (npl <= 32) { FOVEA_SEL(32); }
+      else if (npl <= 48) { FOVEA_SEL(48); }
+      else { FOVEA_SEL(64); }
 #undef FOVEA_SEL
+#undef FOVEA_SEL_C
     } else {
       const size_t sel_smem = static_cast<size_t>(a.m_max) * 4;
       if (sel_smem > 0)

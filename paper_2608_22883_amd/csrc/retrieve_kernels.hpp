@@ -814,20 +814,16 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
 
 
 // ---------------------------------------------------------------------------------
-// Per-node selection and gather for memories of at most 64 * NPL entries and
-// k_max <= 256, one 256-thread block per node.
-// Selection (wave 0 only, no block barriers): each lane holds NPL order keys (entry
-// lane + 64 j).  The k_max-th largest key is found bit by bit (32 steps of a wave-wide
-// ballot count); ties at it are cut by a second bit search over the entry index so the
-// lowest indices win.  Candidates are compacted with ballot prefix counts, sorted
-// descending by (key, -index) in registers (<= 64) or in LDS (<= 256), then prefix
-// masses in fp64, K and the renormalised weights.
-// Gather (all four waves): thread -> (16-byte column chunk, row group); 16 value rows
-// in flight per thread per batch; row groups are summed in a fixed order.
+// Per-node selection by one wave, for memories of at most 64 * NPL entries and
+// k_max <= 256.  Each lane holds NPL order keys (entry lane + 64 j).  The k_max-th
+// largest key is found bit by bit (32 steps of a wave-wide ballot count); ties at it
+// are cut by a second bit search over the entry index so the lowest indices win.
+// Candidates are compacted with ballot prefix counts, sorted descending by
+// (key, -index) in registers (<= 64) or in LDS (<= 256), then prefix masses in fp64,
+// K and the renormalised weights.
 // ---------------------------------------------------------------------------------
 
 constexpr int kWaveSelKmax = 256;
-constexpr int kGatherRows = 32;  // value rows in flight per thread
 
 template <typename T>
 __device__ __forceinline__ void write_invalid_node(const SelectArgs<T>& a, int n, int tid, int nt) {
@@ -858,35 +854,6 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// One gather batch of up to NR value rows (t0, t0 + ng, ...): NR unconditional 16-byte
-// loads (row indices clamped to the last one due), then the weighted sums of the rows
-// that are due.  Advances t0 and left.
-template <typename T, int NR>
-__device__ __forceinline__ void gather_batch(const T* vbase, int d_m, const int* ix, const float* al,
-                                             int& t0, int ng, int& left, int c,
-                                             float (&acc)[Elem<T>::kPer16B]) {
-  constexpr int VEC = Elem<T>::kPer16B;
-  const int nr = min(NR, left);
-  u32x4 raw[NR];
-#pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    const int t = t0 + min(r, nr - 1) * ng;
-    raw[r] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(ix[t]) * d_m + c * VEC);
-  }
-#pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    const float wgt = r < nr ? al[t0 + min(r, nr - 1) * ng] : 0.f;
-    const T* v = reinterpret_cast<const T*>(&raw[r]);
-#pragma unroll
-    for (int x = 0; x < VEC; ++x) {
-      const float f = fmaf(wgt, Elem<T>::to_f32(v[x]), acc[x]);
-      acc[x] = r < nr ? f : acc[x];
-    }
-  }
-  t0 += nr * ng;
-  left -= nr;
 }
 
 // Selection for one node by one wave (see the comment above); writes the selected
@@ -926,36 +893,57 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
     kmax = max(kmax, kv[j]);
     nV += ballot_count(v);
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1)
-    kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), o, kWave)));
+  kmax = wave_max_u32(kmax);
   int K = 0;
   double mass = 0.0;
   if (nV > 0) {
     const float smax = key_to_float(kmax);
+    float ev[NPL];
     double z = 0.0;
 #pragma unroll
-    for (int j = 0; j < NPL; ++j)
-      if (kv[j] != 0u) z += static_cast<double>(expf(key_to_float(kv[j]) - smax));
-    const double Z = wave_sum(z);
+    for (int j = 0; j < NPL; ++j) {
+      ev[j] = kv[j] != 0u ? expf(key_to_float(kv[j]) - smax) : 0.f;
+      z += static_cast<double>(ev[j]);
+    }
+    const double Z = wave_sum_f64(z);
     const int C = min(nV, a.k_max);
     uint32_t thr = 0u;
     int ithr = 0x7FFFFFFF;
     if (nV > a.k_max) {
-      // the k_max-th largest key, bit by bit (masked entries hold 0 and never count)
-      for (int bit = 31; bit >= 0; --bit) {
+      // the k_max-th largest key, bit by bit (masked entries hold 0 and never count);
+      // each lane counts its own entries, and the wave total is read from one ballot
+      // per bit of the lane counts.  The invariant is count(key >= thr) >= k_max; once
+      // it holds with equality, {key >= thr} is already the top k_max and the lower
+      // bits are not needed (thr is then lowered to the smallest selected key so the
+      // tie logic below sees an exact key).
+      bool exact = false;
+      for (int bit = 31; bit >= 0 && !exact; --bit) {
         const uint32_t t = thr | (1u << bit);
+        int c = 0;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) c += kv[j] >= t ? 1 : 0;
         int cnt = 0;
 #pragma unroll
-        for (int j = 0; j < NPL; ++j) cnt += ballot_count(kv[j] >= t);
-        if (cnt >= a.k_max) thr = t;
+        for (int q = 0; (1 << q) <= NPL; ++q) cnt += ballot_count((c >> q) & 1) << q;
+        if (cnt >= a.k_max) {
+          thr = t;
+          exact = cnt == a.k_max;
+        }
+      }
+      if (exact) {
+        uint32_t lo = 0xFFFFFFFFu;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) lo = kv[j] >= thr ? min(lo, kv[j]) : lo;
+        thr = ~wave_max_u32(~lo);
       }
       int gt = 0, eq = 0;
 #pragma unroll
       for (int j = 0; j < NPL; ++j) {
-        gt += ballot_count(kv[j] > thr);
-        eq += ballot_count(kv[j] == thr);
+        gt += kv[j] > thr ? 1 : 0;
+        eq += kv[j] == thr ? 1 : 0;
       }
+      gt = wave_sum_i32(gt);
+      eq = wave_sum_i32(eq);
       const int need = a.k_max - gt;
       if (eq > need) {
         // largest I with #(tied, index < I) < need: the tied entries with index <= I stay
@@ -970,45 +958,63 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
         ithr = I;
       }
     }
-    // compact the C candidates
-    int base = 0;
-    const unsigned long long lt = (1ull << lane) - 1ull;
+    // compact the C candidates (lane-major order; the ranking below orders them)
+    int nsel = 0;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const int i = lane + 64 * j;
+      nsel += (kv[j] != 0u && (nV <= a.k_max || kv[j] > thr || (kv[j] == thr && i <= ithr))) ? 1 : 0;
+    }
+    const int incl_sel = wave_incl_scan_i32(nsel);
+    const int base = __builtin_amdgcn_readlane(incl_sel, 63);
+    int pos = incl_sel - nsel;
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
       const int i = lane + 64 * j;
       const bool sel = kv[j] != 0u && (nV <= a.k_max || kv[j] > thr || (kv[j] == thr && i <= ithr));
-      const unsigned long long m = __ballot(sel);
-      const int pos = base + __popcll(m & lt);
-      if (sel && pos < kWaveSelKmax) cand[pos] = comp_key(kv[j], i);
-      base += __popcll(m);
+      if (sel && pos < kWaveSelKmax) {
+        cand[pos] = comp_key(kv[j], i);
+        alpha_o[pos] = ev[j];  // scratch until the weights are written
+      }
+      pos += sel ? 1 : 0;
     }
     const int Cc = min(C, base);
     wave_lds_sync();
     if (C <= 64) {
-      // sort in registers: lane t ends with rank t
-      unsigned long long x = lane < Cc ? cand[lane] : 0ull;
-#pragma unroll
-      for (int k2 = 2; k2 <= 64; k2 <<= 1) {
-#pragma unroll
-        for (int j2 = k2 >> 1; j2 > 0; j2 >>= 1) {
-          const unsigned long long y = static_cast<unsigned long long>(
-              __shfl_xor(static_cast<long long>(x), j2, kWave));
-          const bool lower = (lane & j2) == 0;
-          const bool desc = (lane & k2) == 0;
-          x = (lower == desc) ? (x > y ? x : y) : (x < y ? x : y);
-        }
-      }
-      const double e = lane < C ? static_cast<double>(expf(key_to_float(static_cast<uint32_t>(x >> 32)) - smax)) : 0.0;
-      double incl = e;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const double y = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += y;
-      }
+      // rank of lane t's candidate = number of larger candidates (keys are distinct);
+      // the fp64 prefix of the masses is summed in rank order by every lane up to its
+      // own rank, and the first rank reaching tau is read from a ballot
+      const unsigned long long x = lane < Cc ? cand[lane] : 0ull;
+      const float ex = lane < Cc ? alpha_o[lane] : 0.f;
+      int rk = 0;
+      for (int u = 0; u < Cc; ++u) rk += cand[u] > x ? 1 : 0;
       wave_lds_sync();
-      cand[lane] = x;
-      pre_s[lane] = incl;
-    } else {
+      if (lane < Cc) pre_s[rk] = static_cast<double>(ex);
+      wave_lds_sync();
+      double incl = 0.0;
+      for (int u = 0; u < Cc; ++u) {
+        const double y = pre_s[u];
+        incl += u <= lane ? y : 0.0;
+      }
+      const double tau = static_cast<double>(a.tau[b]);
+      const unsigned long long hit = __ballot(lane < Cc && incl / Z >= tau);
+      const int K_raw = hit ? __builtin_ctzll(hit) + 1 : (C == nV ? nV : a.k_max + 1);
+      K = min(nV, min(a.k_max, max(a.k_min, K_raw)));
+      const uint64_t iu = static_cast<uint64_t>(__double_as_longlong(incl));
+      const uint32_t ilo = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu), K - 1);
+      const uint32_t ihi = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu >> 32), K - 1);
+      const double sumI = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(ihi) << 32) | ilo));
+      mass = sumI / Z;
+      wave_lds_sync();
+      if (lane < Cc && rk < K) {
+        alpha_o[rk] = static_cast<float>(static_cast<double>(ex) / sumI);
+        idx_o[rk] = static_cast<int>(min(0xFFFFFFFFu - static_cast<uint32_t>(x), static_cast<uint32_t>(M - 1)));
+      }
+      *mass_o = static_cast<float>(mass);
+      return K;
+    }
+    {
+      // larger candidate sets: bitonic sort in LDS, then the prefix
       int P = 128;
       while (P < C) P <<= 1;
       for (int i = Cc + lane; i < P; i += 64) cand[i] = 0ull;
@@ -1070,103 +1076,154 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
   return K;
 }
 
-template <typename T, int NPL>
-__global__ __launch_bounds__(256) void select_block_kernel(SelectArgs<T> a, int n_nodes) {
-  constexpr int VEC = Elem<T>::kPer16B;
-  constexpr int NW = 4;  // nodes per block, one selecting wave each
-  __shared__ unsigned long long cand[NW][kWaveSelKmax];
-  __shared__ double pre_s[NW][kWaveSelKmax];
-  __shared__ float alpha_s[NW][kWaveSelKmax];
-  __shared__ int idx_s[NW][kWaveSelKmax];
-  __shared__ __align__(16) float red[256 * VEC];
-  __shared__ int s_K[NW];
-  __shared__ int64_t s_m0[NW];
-  __shared__ float s_mass[NW];
+// ---------------------------------------------------------------------------------
+// Selection and gather, two nodes per 256-thread block (memories of at most 64 * NPL
+// entries, k_max <= 256, value rows of at most 64 * NCH 16-byte chunks).  Two waves
+// select (above), one node each; then each node's K selected rows are split between
+// two waves (ranks of one parity each), lane l owning chunks l, l + 64, .. of every
+// row, and a batch of up to NR rows is one set of unconditional loads (slots past the
+// wave's rows repeat its last row and are not accumulated), so K <= 2 NR costs one
+// memory round trip.  The two partial sums are added in a fixed order through LDS.
+// ---------------------------------------------------------------------------------
 
-  const int item = xcd_item((n_nodes + NW - 1) / NW);
-  if (item < 0) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  {
-    const int n = item * NW + wave;
+template <typename T, int NCH, int NR>
+__device__ __forceinline__ void gather_rows(const T* __restrict__ vbase, int d_m, int cpr,
+                                            const int* ix, const float* al, int t0, int stride,
+                                            int nr, int lane, float (&acc)[NCH][Elem<T>::kPer16B]) {
+  constexpr int VEC = Elem<T>::kPer16B;
+  u32x4 raw[NR][NCH];
+  int row[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) row[r] = ix[t0 + min(r, nr - 1) * stride];
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int c = min(lane + 64 * u, cpr - 1);
+      raw[r][u] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(row[r]) * d_m + c * VEC);
+    }
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const float w = al[t0 + min(r, nr - 1) * stride];
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const T* v = reinterpret_cast<const T*>(&raw[r][u]);
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) {
+        const float f = fmaf(w, Elem<T>::to_f32(v[x]), acc[u][x]);
+        acc[u][x] = r < nr ? f : acc[u][x];
+      }
+    }
+  }
+}
+
+template <typename T, int NPL, int NCH>
+__global__ __launch_bounds__(256) void select_node_kernel(SelectArgs<T> a, int n_nodes) {
+  constexpr int VEC = Elem<T>::kPer16B;
+  constexpr int NRB = 32 / NCH;  // largest row batch per wave
+  __shared__ unsigned long long cand[2][kWaveSelKmax];
+  __shared__ double pre_s[2][kWaveSelKmax];
+  __shared__ float alpha_s[2][kWaveSelKmax];
+  __shared__ int idx_s[2][kWaveSelKmax];
+  __shared__ __align__(16) float red[2][64 * NCH * VEC];
+  __shared__ int s_K[2];
+  __shared__ int64_t s_m0[2];
+
+  const int pair = xcd_item((n_nodes + 1) / 2);  // a request's nodes share an XCD (and L2)
+  if (pair < 0) return;
+  const int lane = threadIdx.x & 63;
+  // waves are renumbered with the block so that the two selecting waves of the blocks
+  // resident on a CU fall on different SIMDs (a block's wave w runs on SIMD w)
+  const int wave = ((threadIdx.x >> 6) + 2 * ((blockIdx.x >> 3) & 1)) & 3;
+  const int nb = wave & 1;        // the node this wave works on
+  const int half = wave >> 1;     // 0: selects, then gathers even ranks; 1: odd ranks
+  const int n = 2 * pair + nb;
+  const bool live = n < n_nodes;
+  if (half == 0) {
     int K = -1;
     int64_t m0 = 0;
     float mass = 0.f;
-    if (n < n_nodes)
-      K = select_one_node<T, NPL>(a, n, lane, cand[wave], pre_s[wave], alpha_s[wave], idx_s[wave],
-                                  &m0, &mass);
+    if (live) K = select_one_node<T, NPL>(a, n, lane, cand[nb], pre_s[nb], alpha_s[nb], idx_s[nb], &m0, &mass);
     if (lane == 0) {
-      s_K[wave] = K;
-      s_m0[wave] = m0;
-      s_mass[wave] = mass;
+      s_K[nb] = K;
+      s_m0[nb] = m0;
+      if (K >= 0) {
+        if (a.k_out) a.k_out[n] = K;
+        if (a.mass_out) a.mass_out[n] = mass;
+      }
     }
+    if (K >= 0 && a.idx_out)
+      for (int t = lane; t < a.k_max; t += 64) a.idx_out[static_cast<int64_t>(n) * a.k_max + t] = t < K ? idx_s[nb][t] : -1;
   }
   __syncthreads();
-
-  // ---- gather r = sum_t alpha_t u_{idx_t}, node by node: thread -> (chunk, row group) ----
-  const int cpr = a.d_m / VEC;                  // 16-byte chunks per value row
-  const int ng = cpr >= 256 ? 1 : 256 / cpr;    // row groups
-  for (int sn = 0; sn < NW; ++sn) {
-    const int n = item * NW + sn;
-    const int K = s_K[sn];
-    if (n >= n_nodes || K < 0) continue;        // block-uniform
-    const T* vbase = a.values + s_m0[sn] * a.d_m;
-    const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
-    const float* al = alpha_s[sn];
-    const int* ix = idx_s[sn];
-    for (int cp = 0; cp < cpr; cp += 256) {
-      const int c = cp + (tid % (cpr >= 256 ? 256 : cpr));
-      const int rg = cpr >= 256 ? 0 : tid / cpr;
-      const bool live = rg < ng && c < cpr;
-      float acc[VEC];
+  const int K = s_K[nb];
+  const int cpr = a.d_m / VEC;
+  float acc[NCH][VEC];
 #pragma unroll
-      for (int x = 0; x < VEC; ++x) acc[x] = 0.f;
-      if (live) {
-        // rows t = rg, rg + ng, ... below K; the batch size follows the row count so that
-        // every load is unconditional (indices clamped to the last row) and the batch
-        // is one memory round trip
-        int t0 = rg;
-        int left = (K - rg + ng - 1) / ng;
-        while (left > 0) {
-          if (left > 16)
-            gather_batch<T, 32>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
-          else if (left > 8)
-            gather_batch<T, 16>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
-          else if (left > 4)
-            gather_batch<T, 8>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
-          else
-            gather_batch<T, 4>(vbase, a.d_m, ix, al, t0, ng, left, c, acc);
-        }
+  for (int u = 0; u < NCH; ++u)
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) acc[u][x] = 0.f;
+  if (K > 0) {
+    const T* vbase = a.values + s_m0[nb] * a.d_m;
+    const int* ix = idx_s[nb];
+    const float* al = alpha_s[nb];
+    const int mine = K > half ? (K - half + 1) / 2 : 0;  // ranks half, half + 2, ...
+    for (int q0 = 0; q0 < mine;) {
+      const int left = mine - q0;
+      const int t0 = half + 2 * q0;
+      if (left >= NRB) {
+        gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, NRB, lane, acc);
+        q0 += NRB;
+      } else if (left > NRB / 2) {
+        gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+        q0 += left;
+      } else if (left > NRB / 4) {
+        gather_rows<T, NCH, NRB / 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+        q0 += left;
+      } else if (left > 2) {
+        gather_rows<T, NCH, NRB / 4>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+        q0 += left;
+      } else {
+        gather_rows<T, NCH, 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+        q0 += left;
       }
-      if (ng > 1) {
-        if (live) {
-#pragma unroll
-          for (int x = 0; x < VEC; ++x) red[(rg * cpr + c) * VEC + x] = acc[x];
-        }
-        __syncthreads();
-        if (live && rg == 0) {
-          for (int g2 = 1; g2 < ng; ++g2)
-#pragma unroll
-            for (int x = 0; x < VEC; ++x) acc[x] += red[(g2 * cpr + c) * VEC + x];
-        }
-      }
-      if (live && rg == 0) {
-        T outv[VEC];
-#pragma unroll
-        for (int x = 0; x < VEC; ++x) outv[x] = Elem<T>::from_f32(acc[x]);
-        *reinterpret_cast<u32x4*>(a.rT + rbase + c * VEC) = *reinterpret_cast<const u32x4*>(outv);
-        if (a.r_out) {
-#pragma unroll
-          for (int x = 0; x < VEC; ++x) a.r_out[rbase + c * VEC + x] = acc[x];
-        }
-      }
-      if (ng > 1) __syncthreads();
     }
-    if (a.idx_out)
-      for (int tt = tid; tt < a.k_max; tt += 256)
-        a.idx_out[static_cast<int64_t>(n) * a.k_max + tt] = tt < K ? ix[tt] : -1;
-    if (tid == 0) {
-      if (a.k_out) a.k_out[n] = K;
-      if (a.mass_out) a.mass_out[n] = s_mass[sn];
+  }
+  if (half == 1) {
+#pragma unroll
+    for (int u = 0; u < NCH; ++u)
+#pragma unroll
+      for (int x = 0; x < VEC; x += 4)
+        *reinterpret_cast<f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]) =
+            f32x4{acc[u][x], acc[u][x + 1], acc[u][x + 2], acc[u][x + 3]};
+  }
+  __syncthreads();
+  if (half == 1 || K < 0) return;  // K < 0: invalid request, outputs already NaN
+#pragma unroll
+  for (int u = 0; u < NCH; ++u)
+#pragma unroll
+    for (int x = 0; x < VEC; x += 4) {
+      const f32x4 p = *reinterpret_cast<const f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]);
+      acc[u][x] += p[0];
+      acc[u][x + 1] += p[1];
+      acc[u][x + 2] += p[2];
+      acc[u][x + 3] += p[3];
+    }
+  const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
+#pragma unroll
+  for (int u = 0; u < NCH; ++u) {
+    const int c = lane + 64 * u;
+    if (c < cpr) {
+      T outv[VEC];
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) outv[x] = Elem<T>::from_f32(acc[u][x]);
+      *reinterpret_cast<u32x4*>(a.rT + rbase + c * VEC) = *reinterpret_cast<const u32x4*>(outv);
+      if (a.r_out) {
+#pragma unroll
+        for (int x = 0; x < VEC; x += 4)
+          *reinterpret_cast<f32x4*>(a.r_out + rbase + c * VEC + x) =
+              f32x4{acc[u][x], acc[u][x + 1], acc[u][x + 2], acc[u][x + 3]};
+      }
     }
   }
 }
