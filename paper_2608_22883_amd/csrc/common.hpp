@@ -127,6 +127,15 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
   return max(static_cast<uint32_t>(q[0]), static_cast<uint32_t>(q[1]));
 }
 
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int sel = 0; sel < 4; ++sel) v += __uint_as_float(dpp_perm(__float_as_uint(v), sel));
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(static_cast<uint32_t>(p[0])) + __uint_as_float(static_cast<uint32_t>(p[1]));
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(static_cast<uint32_t>(q[0])) + __uint_as_float(static_cast<uint32_t>(q[1]));
+}
+
 __device__ __forceinline__ int wave_sum_i32(int v) {
 #pragma unroll
   for (int sel = 0; sel < 4; ++sel) v += static_cast<int>(dpp_perm(static_cast<uint32_t>(v), sel));

@@ -130,25 +130,28 @@ __global__ __launch_bounds__(256) void corr2_kernel(TileMap tm, int n, const T* 
       });
 }
 
-// RMSNorm of h' in place: h_out = h' / sqrt(mean(h'^2) + eps) * w, one block per row.
+// RMSNorm of h' in place: h_out = h' / sqrt(mean(h'^2) + eps) * w, one wave per row,
+// 16-byte accesses (8 consecutive columns per lane and step); d is a multiple of 64.
 template <typename T>
 __global__ __launch_bounds__(256) void rms_kernel(int n, int d, const float* __restrict__ rms_part,
                                                   const float* __restrict__ w, float eps,
                                                   T* __restrict__ h_out) {
-  __shared__ float s_rstd;
-  const int row = blockIdx.x;
-  const int tid = threadIdx.x;
-  if (tid < 64) {
-    const int n_rp = n_parts(d);
-    float s2 = 0.f;
-    for (int p2 = tid; p2 < n_rp; p2 += 64) s2 += rms_part[static_cast<int64_t>(row) * n_rp + p2];
-    s2 = wave_sum(s2);
-    if (tid == 0) s_rstd = 1.0f / sqrtf(s2 / static_cast<float>(d) + eps);
-  }
-  __syncthreads();
-  const float rstd = s_rstd;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n) return;
+  const int n_rp = n_parts(d);
+  float s2 = 0.f;
+  for (int p2 = lane; p2 < n_rp; p2 += 64) s2 += rms_part[static_cast<int64_t>(row) * n_rp + p2];
+  const float rstd = 1.0f / sqrtf(wave_sum_f32(s2) / static_cast<float>(d) + eps);
   T* hr = h_out + static_cast<int64_t>(row) * d;
-  for (int c = tid; c < d; c += 256) st_f32(hr, c, Elem<T>::to_f32(hr[c]) * rstd * w[c]);
+  for (int c0 = 8 * lane; c0 < d; c0 += 8 * 64) {
+    float v[8], wv[8];
+    load8(hr + c0, v);
+    load8(w + c0, wv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * rstd * wv[e];
+    store8(hr + c0, v);
+  }
 }
 
 // Memory build: [keys | values] = LN(V) [W_K ; W_U]^T with the LayerNorm folded into the

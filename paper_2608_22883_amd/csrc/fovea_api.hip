@@ -410,7 +410,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   // 7. RMSNorm
   if (c->rms_w) {
     ProfScope ps(c, kRms, s);
-    hipLaunchKernelGGL(rms_kernel<T>, dim3(a.n), dim3(256), 0, s, a.n, D.d, rms_part, c->rms_w,
+    hipLaunchKernelGGL(rms_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, D.d, rms_part, c->rms_w,
                        D.rms_eps, h_out);
   }
   FOVEA_HIP(hipGetLastError());

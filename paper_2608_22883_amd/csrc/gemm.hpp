@@ -60,7 +60,7 @@ struct GemmCfg {
   static constexpr int OUT_BYTES = SROWS * SLD * 4;
   static constexpr int PIPE_BYTES = NST * STAGE_BYTES;
   static constexpr int SMEM_BYTES = PIPE_BYTES > OUT_BYTES ? PIPE_BYTES : OUT_BYTES;
-  static_assert(BM == 64 || BM == 128, "block rows");
+  static_assert(BM == 64 || BM == 128 || BM == 256, "block rows");
   static_assert(NST >= 2 && NST <= 5, "pipeline depth");
   static_assert(SMEM_BYTES <= 160 * 1024, "LDS");
 };

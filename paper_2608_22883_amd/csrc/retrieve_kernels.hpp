@@ -41,6 +41,10 @@ __device__ __forceinline__ Extent request_extent(int b, const int64_t* mem_off, 
 // request's node range; node_req[n] = -1 marks a node whose outputs become NaN.
 // ---------------------------------------------------------------------------------
 
+// Rows of up to 64 * kRowChunks 16-byte chunks are held in registers (one load round
+// trip, both LayerNorm passes from registers); longer rows stream in passes.
+constexpr int kRowChunks = 16;
+
 template <typename T>
 __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restrict__ x, int d,
                                                         float eps, float2* __restrict__ stats,
@@ -57,25 +61,56 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
   if (row >= n) return;
   const T* xr = x + static_cast<int64_t>(row) * d;
   const int nch = d / VEC;
-  float s = 0.f;
-  for (int c = lane; c < nch; c += kWave) {
-    const u32x4 raw = *reinterpret_cast<const u32x4*>(xr + c * VEC);
-    const T* v = reinterpret_cast<const T*>(&raw);
+  float mu, var;
+  if (nch <= 64 * kRowChunks) {
+    u32x4 raw[kRowChunks];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) s += Elem<T>::to_f32(v[j]);
-  }
-  const float mu = wave_sum(s) / static_cast<float>(d);
-  float ss = 0.f;
-  for (int c = lane; c < nch; c += kWave) {
-    const u32x4 raw = *reinterpret_cast<const u32x4*>(xr + c * VEC);
-    const T* v = reinterpret_cast<const T*>(&raw);
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) {
-      const float t = Elem<T>::to_f32(v[j]) - mu;
-      ss = fmaf(t, t, ss);
+    for (int u = 0; u < kRowChunks; ++u) {
+      const int c = lane + 64 * u;
+      if (c < nch) raw[u] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
     }
+    float s = 0.f;
+#pragma unroll
+    for (int u = 0; u < kRowChunks; ++u)
+      if (lane + 64 * u < nch) {
+        const T* v = reinterpret_cast<const T*>(&raw[u]);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) s += Elem<T>::to_f32(v[j]);
+      }
+    mu = wave_sum_f32(s) / static_cast<float>(d);
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < kRowChunks; ++u)
+      if (lane + 64 * u < nch) {
+        const T* v = reinterpret_cast<const T*>(&raw[u]);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const float t = Elem<T>::to_f32(v[j]) - mu;
+          ss = fmaf(t, t, ss);
+        }
+      }
+    var = wave_sum_f32(ss) / static_cast<float>(d);
+  } else {
+    float s = 0.f;
+    for (int c = lane; c < nch; c += kWave) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(xr + c * VEC);
+      const T* v = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) s += Elem<T>::to_f32(v[j]);
+    }
+    mu = wave_sum_f32(s) / static_cast<float>(d);
+    float ss = 0.f;
+    for (int c = lane; c < nch; c += kWave) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(xr + c * VEC);
+      const T* v = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        const float t = Elem<T>::to_f32(v[j]) - mu;
+        ss = fmaf(t, t, ss);
+      }
+    }
+    var = wave_sum_f32(ss) / static_cast<float>(d);
   }
-  const float var = wave_sum(ss) / static_cast<float>(d);
   if (lane == 0) stats[row] = make_float2(mu, 1.0f / sqrtf(var + eps));
 
   if (node_off != nullptr && lane == 0) {
