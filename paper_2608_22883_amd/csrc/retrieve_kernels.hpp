@@ -894,39 +894,65 @@ __device__ __forceinline__ void wave_lds_sync() {
 // Selection for one node by one wave (see the comment above); writes the selected
 // indices and renormalised weights to idx_o / alpha_o and returns K (-1 if the node's
 // request is invalid, in which case its outputs have been written as NaN).
+// The keys of one node: validated memory range of its request and the order keys of
+// its scores (entry lane + 64 j in kv[j], 0 for masked or missing entries, the valid
+// ones flagged in bit j of vmask).  Issued ahead of the selection so that the loads of
+// one node overlap the selection of another.
+struct NodeKeys {
+  int b;
+  int M;
+  int64_t m0;
+  bool ok;
+  uint64_t vmask;
+};
+
 template <typename T, int NPL>
-__device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, int lane,
-                                               unsigned long long* cand, double* pre_s,
-                                               float* alpha_o, int* idx_o, int64_t* m0_o,
-                                               float* mass_o) {
-  const int b = a.node_req[n];
-  int64_t m0 = 0, m1 = 0;
-  bool ok = b >= 0;
-  if (ok) {
-    m0 = a.mem_off[b];
-    m1 = a.mem_off[b + 1];
-    if (!(0 <= m0 && m0 <= m1 && m1 <= a.n_mem && m1 - m0 <= a.m_max)) {
-      ok = false;
-      if (lane == 0) atomicOr(a.err, kErrMemOff);
+__device__ __forceinline__ NodeKeys load_node_keys(const SelectArgs<T>& a, int n, int lane,
+                                                   uint32_t (&kv)[NPL]) {
+  NodeKeys r;
+  r.b = a.node_req[n];
+  r.m0 = 0;
+  r.M = 0;
+  r.vmask = 0;
+  r.ok = r.b >= 0;
+  if (r.ok) {
+    const int64_t m0 = a.mem_off[r.b], m1 = a.mem_off[r.b + 1];
+    r.ok = 0 <= m0 && m0 <= m1 && m1 <= a.n_mem && m1 - m0 <= a.m_max;
+    if (r.ok) {
+      r.m0 = m0;
+      r.M = static_cast<int>(m1 - m0);
+    } else if (lane == 0) {
+      atomicOr(a.err, kErrMemOff);
     }
   }
-  if (!ok) {
+  const float* srow = a.S + static_cast<int64_t>(n) * a.m_max;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int i = lane + 64 * j;
+    const bool v = r.ok && i < r.M && (a.valid == nullptr || a.valid[r.m0 + i] != 0);
+    kv[j] = v ? order_key(srow[i]) : 0u;
+    r.vmask |= static_cast<uint64_t>(v) << j;
+  }
+  return r;
+}
+
+template <typename T, int NPL>
+__device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, int lane,
+                                               const NodeKeys& nk, const uint32_t (&kv)[NPL],
+                                               unsigned long long* cand, double* pre_s,
+                                               float* alpha_o, int* idx_o, float* mass_o) {
+  if (!nk.ok) {
     write_invalid_node(a, n, lane, 64);
     return -1;
   }
-  *m0_o = m0;
-  const int M = static_cast<int>(m1 - m0);
-  const float* srow = a.S + static_cast<int64_t>(n) * a.m_max;
-  uint32_t kv[NPL];
+  const int b = nk.b;
+  const int M = nk.M;
   uint32_t kmax = 0;
   int nV = 0;
 #pragma unroll
   for (int j = 0; j < NPL; ++j) {
-    const int i = lane + 64 * j;
-    const bool v = i < M && (a.valid == nullptr || a.valid[m0 + i] != 0);
-    kv[j] = v ? order_key(srow[i]) : 0u;
     kmax = max(kmax, kv[j]);
-    nV += ballot_count(v);
+    nV += ballot_count((nk.vmask >> j) & 1);
   }
   kmax = wave_max_u32(kmax);
   int K = 0;
@@ -1170,94 +1196,101 @@ __global__ __launch_bounds__(256) void select_node_kernel(SelectArgs<T> a, int n
   // waves are renumbered with the block so that the two selecting waves of the blocks
   // resident on a CU fall on different SIMDs (a block's wave w runs on SIMD w)
   const int wave = ((threadIdx.x >> 6) + 2 * ((blockIdx.x >> 3) & 1)) & 3;
-  const int nb = wave & 1;        // the node this wave works on
-  const int half = wave >> 1;     // 0: selects, then gathers even ranks; 1: odd ranks
-  const int n = 2 * pair + nb;
-  const bool live = n < n_nodes;
-  if (half == 0) {
-    int K = -1;
-    int64_t m0 = 0;
-    float mass = 0.f;
-    if (live) K = select_one_node<T, NPL>(a, n, lane, cand[nb], pre_s[nb], alpha_s[nb], idx_s[nb], &m0, &mass);
-    if (lane == 0) {
-      s_K[nb] = K;
-      s_m0[nb] = m0;
-      if (K >= 0) {
-        if (a.k_out) a.k_out[n] = K;
-        if (a.mass_out) a.mass_out[n] = mass;
-      }
-    }
-    if (K >= 0 && a.idx_out)
-      for (int t = lane; t < a.k_max; t += 64) a.idx_out[static_cast<int64_t>(n) * a.k_max + t] = t < K ? idx_s[nb][t] : -1;
-  }
-  __syncthreads();
-  const int K = s_K[nb];
+  const int nb = wave & 1;     // the node of the pair this wave works on
+  const int half = wave >> 1;  // 0: selects, then gathers even ranks; 1: odd ranks
   const int cpr = a.d_m / VEC;
-  float acc[NCH][VEC];
-#pragma unroll
-  for (int u = 0; u < NCH; ++u)
-#pragma unroll
-    for (int x = 0; x < VEC; ++x) acc[u][x] = 0.f;
-  if (K > 0) {
-    const T* vbase = a.values + s_m0[nb] * a.d_m;
-    const int* ix = idx_s[nb];
-    const float* al = alpha_s[nb];
-    const int mine = K > half ? (K - half + 1) / 2 : 0;  // ranks half, half + 2, ...
-    for (int q0 = 0; q0 < mine;) {
-      const int left = mine - q0;
-      const int t0 = half + 2 * q0;
-      if (left >= NRB) {
-        gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, NRB, lane, acc);
-        q0 += NRB;
-      } else if (left > NRB / 2) {
-        gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
-        q0 += left;
-      } else if (left > NRB / 4) {
-        gather_rows<T, NCH, NRB / 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
-        q0 += left;
-      } else if (left > 2) {
-        gather_rows<T, NCH, NRB / 4>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
-        q0 += left;
-      } else {
-        gather_rows<T, NCH, 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
-        q0 += left;
+  {
+    const int n = 2 * pair + nb;
+    const bool live = n < n_nodes;
+    if (half == 0) {
+      uint32_t kv[NPL];
+      NodeKeys nk;
+      nk.ok = false;
+      nk.m0 = 0;
+      if (live) nk = load_node_keys<T, NPL>(a, n, lane, kv);
+      int K = -1;
+      float mass = 0.f;
+      if (live) K = select_one_node<T, NPL>(a, n, lane, nk, kv, cand[nb], pre_s[nb], alpha_s[nb], idx_s[nb], &mass);
+      if (lane == 0) {
+        s_K[nb] = K;
+        s_m0[nb] = nk.m0;
+        if (K >= 0) {
+          if (a.k_out) a.k_out[n] = K;
+          if (a.mass_out) a.mass_out[n] = mass;
+        }
       }
+      if (K >= 0 && a.idx_out)
+        for (int t = lane; t < a.k_max; t += 64) a.idx_out[static_cast<int64_t>(n) * a.k_max + t] = t < K ? idx_s[nb][t] : -1;
     }
-  }
-  if (half == 1) {
+    __syncthreads();
+    const int K = s_K[nb];
+    float acc[NCH][VEC];
 #pragma unroll
     for (int u = 0; u < NCH; ++u)
 #pragma unroll
-      for (int x = 0; x < VEC; x += 4)
-        *reinterpret_cast<f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]) =
-            f32x4{acc[u][x], acc[u][x + 1], acc[u][x + 2], acc[u][x + 3]};
-  }
-  __syncthreads();
-  if (half == 1 || K < 0) return;  // K < 0: invalid request, outputs already NaN
-#pragma unroll
-  for (int u = 0; u < NCH; ++u)
-#pragma unroll
-    for (int x = 0; x < VEC; x += 4) {
-      const f32x4 p = *reinterpret_cast<const f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]);
-      acc[u][x] += p[0];
-      acc[u][x + 1] += p[1];
-      acc[u][x + 2] += p[2];
-      acc[u][x + 3] += p[3];
+      for (int x = 0; x < VEC; ++x) acc[u][x] = 0.f;
+    if (K > 0) {
+      const T* vbase = a.values + s_m0[nb] * a.d_m;
+      const int* ix = idx_s[nb];
+      const float* al = alpha_s[nb];
+      const int mine = K > half ? (K - half + 1) / 2 : 0;  // ranks half, half + 2, ...
+      for (int q0 = 0; q0 < mine;) {
+        const int left = mine - q0;
+        const int t0 = half + 2 * q0;
+        if (left >= NRB) {
+          gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, NRB, lane, acc);
+          q0 += NRB;
+        } else if (left > NRB / 2) {
+          gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          q0 += left;
+        } else if (left > NRB / 4) {
+          gather_rows<T, NCH, NRB / 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          q0 += left;
+        } else if (left > 2) {
+          gather_rows<T, NCH, NRB / 4>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          q0 += left;
+        } else {
+          gather_rows<T, NCH, 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          q0 += left;
+        }
+      }
     }
-  const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
+    if (half == 1) {
 #pragma unroll
-  for (int u = 0; u < NCH; ++u) {
-    const int c = lane + 64 * u;
-    if (c < cpr) {
-      T outv[VEC];
-#pragma unroll
-      for (int x = 0; x < VEC; ++x) outv[x] = Elem<T>::from_f32(acc[u][x]);
-      *reinterpret_cast<u32x4*>(a.rT + rbase + c * VEC) = *reinterpret_cast<const u32x4*>(outv);
-      if (a.r_out) {
+      for (int u = 0; u < NCH; ++u)
 #pragma unroll
         for (int x = 0; x < VEC; x += 4)
-          *reinterpret_cast<f32x4*>(a.r_out + rbase + c * VEC + x) =
+          *reinterpret_cast<f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]) =
               f32x4{acc[u][x], acc[u][x + 1], acc[u][x + 2], acc[u][x + 3]};
+    }
+    __syncthreads();
+    if (half == 0 && K >= 0) {  // K < 0: invalid request, outputs already NaN
+#pragma unroll
+      for (int u = 0; u < NCH; ++u)
+#pragma unroll
+        for (int x = 0; x < VEC; x += 4) {
+          const f32x4 p = *reinterpret_cast<const f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]);
+          acc[u][x] += p[0];
+          acc[u][x + 1] += p[1];
+          acc[u][x + 2] += p[2];
+          acc[u][x + 3] += p[3];
+        }
+      const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) {
+        const int c = lane + 64 * u;
+        if (c < cpr) {
+          T outv[VEC];
+#pragma unroll
+          for (int x = 0; x < VEC; ++x) outv[x] = Elem<T>::from_f32(acc[u][x]);
+          *reinterpret_cast<u32x4*>(a.rT + rbase + c * VEC) = *reinterpret_cast<const u32x4*>(outv);
+          if (a.r_out) {
+#pragma unroll
+            for (int x = 0; x < VEC; x += 4)
+              *reinterpret_cast<f32x4*>(a.r_out + rbase + c * VEC + x) =
+                  f32x4{acc[u][x], acc[u][x + 1], acc[u][x + 2], acc[u][x + 3]};
+          }
+        }
       }
     }
   }
