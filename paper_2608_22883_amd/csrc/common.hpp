@@ -21,12 +21,29 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// Round to nearest, ties to even; NaN stays a quiet NaN, overflow rounds to inf.
+// Round to nearest, ties to even; NaN stays a quiet NaN, overflow rounds to inf.  The
+// packed and float-valued forms below use the gfx950 conversion instruction (same
+// rounding); the bit-level form is kept for the selection kernel, whose register
+// allocation is tighter with it.
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+__device__ __forceinline__ float bf16_round(float f) {
+  return static_cast<float>(static_cast<__bf16>(f));
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   uint32_t u = __float_as_uint(f);
   if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
   u += 0x7fffu + ((u >> 16) & 1u);
   return static_cast<uint16_t>(u >> 16);
+}
+
+// Two values rounded to bf16 and packed (lo in the low half), one instruction.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  bf16x2_t r;
+  r[0] = static_cast<__bf16>(lo);
+  r[1] = static_cast<__bf16>(hi);
+  return __builtin_bit_cast(uint32_t, r);
 }
 
 // Storage element traits: T is float (fp32 storage) or bf16_t (bf16 storage).
@@ -82,9 +99,7 @@ __device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
 __device__ __forceinline__ void store8(bf16_t* p, const float (&x)[8]) {
   u32x4 a;
 #pragma unroll
-  for (int e = 0; e < 4; ++e)
-    a[e] = static_cast<uint32_t>(f32_to_bf16_bits(x[2 * e])) |
-           (static_cast<uint32_t>(f32_to_bf16_bits(x[2 * e + 1])) << 16);
+  for (int e = 0; e < 4; ++e) a[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
   *reinterpret_cast<u32x4*>(p) = a;
 }
 

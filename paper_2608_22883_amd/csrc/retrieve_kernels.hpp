@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __r
           float hi[8], lo[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            hi[e] = bf16_bits_to_f32(f32_to_bf16_bits(val[e]));
+            hi[e] = bf16_round(val[e]);
             lo[e] = val[e] - hi[e];
           }
           store8(q + o, hi);
