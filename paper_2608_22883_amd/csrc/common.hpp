@@ -216,6 +216,23 @@ __device__ __forceinline__ f32x4 mfma_bf16_16x16x32(bf16x8 a, bf16x8 b, f32x4 c)
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// In-place accumulation: the accumulator is pinned to one register tuple (the
+// compiler's own allocation of loop-carried accumulators otherwise rotates them and
+// inserts copies that drain the matrix pipeline every iteration).  Back-to-back MFMAs
+// on the same accumulator are interlocked in hardware; vector reads of the results
+// must be preceded by mfma_results_ready().
+__device__ __forceinline__ void mfma_bf16_16x16x32_acc(f32x4& c, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+
+// Wait states between the last in-place MFMA and vector reads of its results (more
+// than the longest MFMA's latency); the scheduling barrier keeps the compiler from
+// moving the reads above the padding.
+__device__ __forceinline__ void mfma_results_ready() {
+  asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }

@@ -208,38 +208,53 @@ __device__ __forceinline__ void gemm_mainloop_dma(f32x4 (&acc)[C::TM][C::TN],
     wait_vmcnt<(NST - 2) * NI>();
     lds_barrier();
     const unsigned char* st = smem + (kt % NST) * C::STAGE_BYTES;
+    const int knext = min(kt + NST - 1, nk - 1), snext = (kt + NST - 1) % NST;
     bf16x8 af[2][TM], bf[2][TN];
+    // fragment r (0 .. TM + TN - 1) of half h, in the order the i-major MFMAs first use
+    // them: A0, B0 .. B(TN-1), A1 .. A(TM-1)
+    auto read_frag = [&](int h, int r) {
+      if (r == 0)
+        af[h][0] = *reinterpret_cast<const bf16x8*>(st + fa[h]);
+      else if (r <= TN)
+        bf[h][r - 1] = *reinterpret_cast<const bf16x8*>(st + fb[h] + (r - 1) * 16 * 128);
+      else
+        af[h][r - TN] = *reinterpret_cast<const bf16x8*>(st + fa[h] + (r - TN) * 16 * 128);
+    };
+    // load q (0 .. NI - 1) of the tile knext into stage snext
+    auto issue_one = [&](int q) {
+      unsigned char* sn = smem + snext * C::STAGE_BYTES;
+      const int k0 = knext * C::BK;
+      if (q < C::A_DMA)
+        __builtin_amdgcn_global_load_lds(ga[q] + k0, (lds_void_ptr)(sn + da[q]), 16, 0, 0);
+      else
+        __builtin_amdgcn_global_load_lds(gb[q - C::A_DMA] + k0, (lds_void_ptr)(sn + db[q - C::A_DMA]), 16, 0, 0);
+    };
+    // first half's reads; then its MFMAs, each followed by one of the second half's
+    // reads and then by one of the loads of a later tile; the compiler barriers keep
+    // every LDS access and load at its place between the MFMAs
+    constexpr int NH = TM + TN;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      af[h][0] = *reinterpret_cast<const bf16x8*>(st + fa[h]);
+    for (int r = 0; r < NH; ++r) read_frag(0, r);
+    asm volatile("" ::: "memory");
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bf[h][j] = *reinterpret_cast<const bf16x8*>(st + fb[h] + j * 16 * 128);
-#pragma unroll
-      for (int i = 1; i < TM; ++i) af[h][i] = *reinterpret_cast<const bf16x8*>(st + fa[h] + i * 16 * 128);
+    for (int m = 0; m < TM * TN; ++m) {
+      mfma_bf16_16x16x32_acc(acc[m / TN][m % TN], af[0][m / TN], bf[0][m % TN]);
+      if (m < NH)
+        read_frag(1, m);
+      else if (m - NH < NI)
+        issue_one(m - NH);
+      asm volatile("" ::: "memory");
     }
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int q = TM * TN - NH; q < NI; ++q) issue_one(q);
+    asm volatile("" ::: "memory");
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16_16x16x32(af[h][i], bf[h][j], acc[i][j]);
-    issue(min(kt + NST - 1, nk - 1), (kt + NST - 1) % NST);
-    constexpr int NH = TM + TN;  // reads per k half
-    __builtin_amdgcn_sched_group_barrier(0x100, NH, 0);
-#pragma unroll
-    for (int t = 0; t < NH; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-#pragma unroll
-    for (int t = 0; t < NI; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM * TN - NH - NI, 0);
+    for (int m = 0; m < TM * TN; ++m)
+      mfma_bf16_16x16x32_acc(acc[m / TN][m % TN], af[1][m / TN], bf[1][m % TN]);
   }
   // the extra loads of the last steps land before the LDS is reused
   wait_vmcnt<0>();
+  mfma_results_ready();
   lds_barrier();
 }
 
