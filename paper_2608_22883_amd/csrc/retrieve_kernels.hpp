@@ -61,6 +61,14 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
   if (row >= n) return;
   const T* xr = x + static_cast<int64_t>(row) * d;
   const int nch = d / VEC;
+  // request lookup operands, loaded together with the row
+  int off_v = 0, dep_v = 0;
+  float tau_v = 0.f;
+  if (node_off != nullptr && B < 64) {
+    off_v = node_off[min(lane, B)];
+    tau_v = tau[min(lane, B - 1)];
+    dep_v = depth[row];
+  }
   float mu, var;
   if (nch <= 64 * kRowChunks) {
     u32x4 raw[kRowChunks];
@@ -113,23 +121,43 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
   }
   if (lane == 0) stats[row] = make_float2(mu, 1.0f / sqrtf(var + eps));
 
-  if (node_off != nullptr && lane == 0) {
-    // largest b with node_off[b] <= row (a fixed number of steps even if the offsets are bad)
-    int lo = 0, hi = B - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (node_off[mid] <= row) lo = mid; else hi = mid - 1;
+  if (node_off != nullptr) {
+    // largest b with node_off[b] <= row (a fixed number of steps even if the offsets
+    // are bad); for B < 64 the offsets, tau and depth were loaded with the row, and the
+    // search reads them across lanes
+    int b, t0, t1, dep;
+    float tb;
+    if (B < 64) {
+      int lo = 0, hi = B - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (__builtin_amdgcn_readlane(off_v, mid) <= row) lo = mid; else hi = mid - 1;
+      }
+      b = lo;
+      t0 = __builtin_amdgcn_readlane(off_v, b);
+      t1 = __builtin_amdgcn_readlane(off_v, b + 1);
+      tb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(tau_v), b));
+      dep = dep_v;
+    } else {
+      int lo = 0, hi = B - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (node_off[mid] <= row) lo = mid; else hi = mid - 1;
+      }
+      b = lo;
+      t0 = node_off[b];
+      t1 = node_off[b + 1];
+      tb = tau[b];
+      dep = depth[row];
     }
-    const int b = lo;
-    const int t0 = node_off[b], t1 = node_off[b + 1];
-    uint32_t bad = 0;
-    if (!(0 <= t0 && t0 <= row && row < t1 && t1 <= n && t1 - t0 <= t_max)) bad |= kErrNodeOff;
-    const int dep = depth[row];
-    if (dep < 0 || dep >= n_depth) bad |= kErrDepth;
-    const float tb = tau[b];
-    if (!(tb >= 0.f && tb <= 1.f)) bad |= kErrTau;
-    node_req[row] = bad ? -1 : b;
-    if (bad) atomicOr(err, bad);
+    if (lane == 0) {
+      uint32_t bad = 0;
+      if (!(0 <= t0 && t0 <= row && row < t1 && t1 <= n && t1 - t0 <= t_max)) bad |= kErrNodeOff;
+      if (dep < 0 || dep >= n_depth) bad |= kErrDepth;
+      if (!(tb >= 0.f && tb <= 1.f)) bad |= kErrTau;
+      node_req[row] = bad ? -1 : b;
+      if (bad) atomicOr(err, bad);
+    }
   }
 }
 
