@@ -173,6 +173,29 @@ __device__ __forceinline__ int wave_incl_scan_i32(int v) {
   return v;
 }
 
+// Lanes shifted by a DPP row control; lanes without a source (row edge, masked rows or
+// banks) read +0.0.
+template <int CTRL, int ROW_MASK, int BANK_MASK>
+__device__ __forceinline__ double dpp_shift_f64(double v) {
+  const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, static_cast<uint32_t>(u), CTRL, ROW_MASK, BANK_MASK, false);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, static_cast<uint32_t>(u >> 32), CTRL, ROW_MASK, BANK_MASK, false);
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+// Inclusive prefix sum over the wave in fp64 (same steps as the integer scan above).
+__device__ __forceinline__ double wave_incl_scan_f64(double v) {
+  const double x = v;
+  v += dpp_shift_f64<0x111, 0xF, 0xF>(x);
+  v += dpp_shift_f64<0x112, 0xF, 0xF>(x);
+  v += dpp_shift_f64<0x113, 0xF, 0xF>(x);
+  v += dpp_shift_f64<0x114, 0xF, 0xE>(v);
+  v += dpp_shift_f64<0x118, 0xF, 0xC>(v);
+  v += dpp_shift_f64<0x142, 0xA, 0xF>(v);
+  v += dpp_shift_f64<0x143, 0xC, 0xF>(v);
+  return v;
+}
+
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int sel = 0; sel < 4; ++sel) {

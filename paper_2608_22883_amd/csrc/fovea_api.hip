@@ -62,7 +62,7 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 // Byte offsets of the retrieve_fuse workspace regions.
 struct WsLayout {
-  size_t node_req, stats, q, P, S, rT, a_c, gate_part, rms_part, total;
+  size_t node_req, info, stats, q, P, S, rT, a_c, gate_part, rms_part, total;
 };
 
 WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
@@ -70,6 +70,7 @@ WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
   WsLayout L;
   size_t o = 0;
   L.node_req = o; o = align_up(o + n * 4);
+  L.info = o; o = align_up(o + n * sizeof(NodeInfo));
   L.stats = o; o = align_up(o + n * 8);
   L.q = o; o = align_up(o + n * dm.d_m * (dm.dtype == FOVEA_BF16 ? 2 * kQSplitBf16 : 4));
   L.P = o; o = align_up(o + n * 2 * dm.d_c * 4);
@@ -196,8 +197,9 @@ fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* val
     hipLaunchKernelGGL(row_stats_kernel<T>, dim3((n + 3) / 4), dim3(256), 0, s, n,
                        static_cast<const T*>(V), D.d_v, D.ln_eps, c->build_stats,
                        static_cast<const int32_t*>(nullptr), 0, static_cast<const int32_t*>(nullptr),
-                       0, 0, static_cast<const float*>(nullptr), static_cast<int32_t*>(nullptr),
-                       c->err);
+                       0, 0, static_cast<const float*>(nullptr),
+                       static_cast<const int64_t*>(nullptr), int64_t{0}, 0,
+                       static_cast<int32_t*>(nullptr), static_cast<NodeInfo*>(nullptr), c->err);
   }
   using C = MemCfg<T>;
   const TileMap tm = make_tile_map((n + C::BM - 1) / C::BM, (2 * D.d_m + C::BN - 1) / C::BN,
@@ -283,6 +285,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   const fovea_dims& D = c->dims;
   const WsLayout L = ws_layout(D, a.n, a.m_max);
   int32_t* node_req = reinterpret_cast<int32_t*>(a.ws + L.node_req);
+  NodeInfo* info = reinterpret_cast<NodeInfo*>(a.ws + L.info);
   float2* stats = reinterpret_cast<float2*>(a.ws + L.stats);
   T* q = reinterpret_cast<T*>(a.ws + L.q);
   float* P = reinterpret_cast<float*>(a.ws + L.P);
@@ -298,7 +301,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     ProfScope ps(c, kRowStats, s);
     hipLaunchKernelGGL(row_stats_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, h, D.d,
                        D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
-                       node_req, c->err);
+                       a.mem_off, a.n_mem, a.m_max, node_req, info, c->err);
   }
   // 2. everything that depends on h alone: q = W_Q (LN(h) + E_dep[l]) and P = h W1h^T
   {
@@ -339,6 +342,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   sa.n_mem = a.n_mem;
   sa.m_max = a.m_max;
   sa.node_req = node_req;
+  sa.info = info;
   sa.tau = a.tau;
   sa.valid = a.valid;
   sa.values = static_cast<const T*>(a.values);

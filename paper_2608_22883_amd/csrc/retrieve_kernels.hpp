@@ -45,6 +45,15 @@ __device__ __forceinline__ Extent request_extent(int b, const int64_t* mem_off, 
 // trip, both LayerNorm passes from registers); longer rows stream in passes.
 constexpr int kRowChunks = 16;
 
+// Per-node view of its request, written by the statistics kernel so that the selection
+// reads it with one load: the request's memory range and tau.  M < 0 marks a node whose
+// offsets, depth, tau or memory range failed validation (the error bits are set).
+struct NodeInfo {
+  int64_t m0;
+  int32_t M;
+  float tau;
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restrict__ x, int d,
                                                         float eps, float2* __restrict__ stats,
@@ -53,7 +62,10 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
                                                         const int32_t* __restrict__ node_off,
                                                         int B, int t_max,
                                                         const float* __restrict__ tau,
+                                                        const int64_t* __restrict__ mem_off,
+                                                        int64_t n_mem, int m_max,
                                                         int32_t* __restrict__ node_req,
+                                                        NodeInfo* __restrict__ info,
                                                         uint32_t* err) {
   constexpr int VEC = Elem<T>::kPer16B;
   const int lane = threadIdx.x & 63;
@@ -64,9 +76,11 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
   // request lookup operands, loaded together with the row
   int off_v = 0, dep_v = 0;
   float tau_v = 0.f;
+  int64_t mem_v = 0;
   if (node_off != nullptr && B < 64) {
     off_v = node_off[min(lane, B)];
     tau_v = tau[min(lane, B - 1)];
+    mem_v = mem_off[min(lane, B)];
     dep_v = depth[row];
   }
   float mu, var;
@@ -127,6 +141,7 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
     // search reads them across lanes
     int b, t0, t1, dep;
     float tb;
+    int64_t m0, m1;
     if (B < 64) {
       int lo = 0, hi = B - 1;
       while (lo < hi) {
@@ -137,6 +152,11 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
       t0 = __builtin_amdgcn_readlane(off_v, b);
       t1 = __builtin_amdgcn_readlane(off_v, b + 1);
       tb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(tau_v), b));
+      const uint64_t mu = static_cast<uint64_t>(mem_v);
+      m0 = static_cast<int64_t>((static_cast<uint64_t>(__builtin_amdgcn_readlane(static_cast<uint32_t>(mu >> 32), b)) << 32) |
+                                __builtin_amdgcn_readlane(static_cast<uint32_t>(mu), b));
+      m1 = static_cast<int64_t>((static_cast<uint64_t>(__builtin_amdgcn_readlane(static_cast<uint32_t>(mu >> 32), b + 1)) << 32) |
+                                __builtin_amdgcn_readlane(static_cast<uint32_t>(mu), b + 1));
       dep = dep_v;
     } else {
       int lo = 0, hi = B - 1;
@@ -148,6 +168,8 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
       t0 = node_off[b];
       t1 = node_off[b + 1];
       tb = tau[b];
+      m0 = mem_off[b];
+      m1 = mem_off[b + 1];
       dep = depth[row];
     }
     if (lane == 0) {
@@ -156,6 +178,14 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
       if (dep < 0 || dep >= n_depth) bad |= kErrDepth;
       if (!(tb >= 0.f && tb <= 1.f)) bad |= kErrTau;
       node_req[row] = bad ? -1 : b;
+      // the memory range is checked only for nodes that map to a request
+      const bool mem_ok = 0 <= m0 && m0 <= m1 && m1 <= n_mem && m1 - m0 <= m_max;
+      if (!bad && !mem_ok) bad |= kErrMemOff;
+      NodeInfo ni;
+      ni.m0 = mem_ok ? m0 : 0;
+      ni.M = bad ? -1 : static_cast<int32_t>(m1 - m0);
+      ni.tau = tb;
+      info[row] = ni;
       if (bad) atomicOr(err, bad);
     }
   }
@@ -552,6 +582,7 @@ struct SelectArgs {
   int64_t n_mem;
   int m_max;
   const int32_t* node_req;
+  const NodeInfo* info;
   const float* tau;
   const uint8_t* valid;
   const T* values;
@@ -879,8 +910,8 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
 // ---------------------------------------------------------------------------------
 // Per-node selection by one wave, for memories of at most 64 * NPL entries and
 // k_max <= 256.  Each lane holds NPL order keys (entry lane + 64 j).  The k_max-th
-// largest key is found bit by bit (32 steps of a wave-wide ballot count); ties at it
-// are cut by a second bit search over the entry index so the lowest indices win.
+// largest key is found bit by bit (at most 32 steps of ballot counts); ties at it are
+// cut by a second bit search over the entry index so the lowest indices win.
 // Candidates are compacted with ballot prefix counts, sorted descending by
 // (key, -index) in registers (<= 64) or in LDS (<= 256), then prefix masses in fp64,
 // K and the renormalised weights.
@@ -919,17 +950,14 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Selection for one node by one wave (see the comment above); writes the selected
-// indices and renormalised weights to idx_o / alpha_o and returns K (-1 if the node's
-// request is invalid, in which case its outputs have been written as NaN).
-// The keys of one node: validated memory range of its request and the order keys of
-// its scores (entry lane + 64 j in kv[j], 0 for masked or missing entries, the valid
-// ones flagged in bit j of vmask).  Issued ahead of the selection so that the loads of
-// one node overlap the selection of another.
+// The keys of one node: its request's memory range and tau (validated by the statistics
+// kernel) and the order keys of its scores (entry lane + 64 j in kv[j], 0 for masked or
+// missing entries, the valid ones flagged in bit j of vmask).  The score row and the
+// node record are independent loads, so both are in flight together.
 struct NodeKeys {
-  int b;
   int M;
   int64_t m0;
+  float tau;
   bool ok;
   uint64_t vmask;
 };
@@ -937,33 +965,35 @@ struct NodeKeys {
 template <typename T, int NPL>
 __device__ __forceinline__ NodeKeys load_node_keys(const SelectArgs<T>& a, int n, int lane,
                                                    uint32_t (&kv)[NPL]) {
-  NodeKeys r;
-  r.b = a.node_req[n];
-  r.m0 = 0;
-  r.M = 0;
-  r.vmask = 0;
-  r.ok = r.b >= 0;
-  if (r.ok) {
-    const int64_t m0 = a.mem_off[r.b], m1 = a.mem_off[r.b + 1];
-    r.ok = 0 <= m0 && m0 <= m1 && m1 <= a.n_mem && m1 - m0 <= a.m_max;
-    if (r.ok) {
-      r.m0 = m0;
-      r.M = static_cast<int>(m1 - m0);
-    } else if (lane == 0) {
-      atomicOr(a.err, kErrMemOff);
-    }
-  }
   const float* srow = a.S + static_cast<int64_t>(n) * a.m_max;
+  float sv[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) sv[j] = a.m_max > 0 ? srow[min(lane + 64 * j, a.m_max - 1)] : 0.f;
+  const NodeInfo inf = a.info[n];
+  NodeKeys r;
+  r.ok = inf.M >= 0;
+  r.M = r.ok ? inf.M : 0;
+  r.m0 = inf.m0;
+  r.tau = inf.tau;
+  r.vmask = 0;
 #pragma unroll
   for (int j = 0; j < NPL; ++j) {
     const int i = lane + 64 * j;
-    const bool v = r.ok && i < r.M && (a.valid == nullptr || a.valid[r.m0 + i] != 0);
-    kv[j] = v ? order_key(srow[i]) : 0u;
+    const bool v = i < r.M && (a.valid == nullptr || a.valid[r.m0 + i] != 0);
+    kv[j] = v ? order_key(sv[j]) : 0u;
     r.vmask |= static_cast<uint64_t>(v) << j;
   }
   return r;
 }
 
+// Selection for one node by one wave: writes the selected indices and renormalised
+// weights (rank order) to idx_o / alpha_o and returns K (-1 if the node is invalid, in
+// which case its outputs have been written as NaN).
+//  * the top min(nV, k_max) keys are found bit by bit (the k_max-th largest key), each
+//    count read from one ballot per key slot;
+//  * the candidates are compacted, ranked by counting (keys are made distinct by the
+//    index), their masses placed in rank order and summed by a wave prefix scan in fp64;
+//  * K_raw is the first rank whose prefix reaches tau Z, clamped to [k_min, k_max].
 template <typename T, int NPL>
 __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, int lane,
                                                const NodeKeys& nk, const uint32_t (&kv)[NPL],
@@ -973,16 +1003,15 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
     write_invalid_node(a, n, lane, 64);
     return -1;
   }
-  const int b = nk.b;
   const int M = nk.M;
-  uint32_t kmax = 0;
+  uint32_t lmax = 0;
   int nV = 0;
 #pragma unroll
   for (int j = 0; j < NPL; ++j) {
-    kmax = max(kmax, kv[j]);
+    lmax = max(lmax, kv[j]);
     nV += ballot_count((nk.vmask >> j) & 1);
   }
-  kmax = wave_max_u32(kmax);
+  const uint32_t kmax = __builtin_amdgcn_readfirstlane(wave_max_u32(lmax));
   int K = 0;
   double mass = 0.0;
   if (nV > 0) {
@@ -999,46 +1028,44 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
     uint32_t thr = 0u;
     int ithr = 0x7FFFFFFF;
     if (nV > a.k_max) {
-      // the k_max-th largest key, bit by bit (masked entries hold 0 and never count);
-      // each lane counts its own entries, and the wave total is read from one ballot
-      // per bit of the lane counts.  The invariant is count(key >= thr) >= k_max; once
-      // it holds with equality, {key >= thr} is already the top k_max and the lower
-      // bits are not needed (thr is then lowered to the smallest selected key so the
-      // tie logic below sees an exact key).
+      // the k_max-th largest key, bit by bit, under the invariant count(key >= thr) >=
+      // k_max (masked entries hold 0; every tested threshold is >= 1, so they never
+      // count).  With k_max <= 64 the search starts below the bits that the largest key
+      // shares with the smallest lane maximum: each lane holds a key >= that minimum, so
+      // at least 64 keys reach the shared prefix.  Once the count equals k_max the set
+      // {key >= thr} is the top k_max and the lower bits are not needed.
+      int bit = 31;
+      if (a.k_max <= 64) {
+        const uint32_t t0 = __builtin_amdgcn_readfirstlane(~wave_max_u32(~lmax));
+        const uint32_t diff = t0 ^ kmax;
+        bit = diff != 0u ? 31 - __builtin_clz(diff) : -1;
+        thr = diff != 0u ? (kmax & ~((2u << bit) - 1u)) : kmax;
+      }
       bool exact = false;
-      for (int bit = 31; bit >= 0 && !exact; --bit) {
+      for (; bit >= 0; --bit) {
         const uint32_t t = thr | (1u << bit);
-        int c = 0;
-#pragma unroll
-        for (int j = 0; j < NPL; ++j) c += kv[j] >= t ? 1 : 0;
         int cnt = 0;
 #pragma unroll
-        for (int q = 0; (1 << q) <= NPL; ++q) cnt += ballot_count((c >> q) & 1) << q;
+        for (int j = 0; j < NPL; ++j) cnt += ballot_count(kv[j] >= t);
         if (cnt >= a.k_max) {
           thr = t;
-          exact = cnt == a.k_max;
+          if (cnt == a.k_max) {
+            exact = true;
+            break;
+          }
         }
       }
-      if (exact) {
-        uint32_t lo = 0xFFFFFFFFu;
+      if (!exact) {
+        // thr is the k_max-th largest key itself and more than k_max keys reach it:
+        // keep the tied entries with the lowest indices.  I is the largest index bound
+        // with #(tied, index < I) < need, so the tied entries with index <= I stay.
+        int gt = 0;
 #pragma unroll
-        for (int j = 0; j < NPL; ++j) lo = kv[j] >= thr ? min(lo, kv[j]) : lo;
-        thr = ~wave_max_u32(~lo);
-      }
-      int gt = 0, eq = 0;
-#pragma unroll
-      for (int j = 0; j < NPL; ++j) {
-        gt += kv[j] > thr ? 1 : 0;
-        eq += kv[j] == thr ? 1 : 0;
-      }
-      gt = wave_sum_i32(gt);
-      eq = wave_sum_i32(eq);
-      const int need = a.k_max - gt;
-      if (eq > need) {
-        // largest I with #(tied, index < I) < need: the tied entries with index <= I stay
+        for (int j = 0; j < NPL; ++j) gt += ballot_count(kv[j] > thr);
+        const int need = a.k_max - gt;
         int I = 0;
-        for (int bit = 14; bit >= 0; --bit) {
-          const int t = I + (1 << bit);
+        for (int b2 = 14; b2 >= 0; --b2) {
+          const int t = I + (1 << b2);
           int f = 0;
 #pragma unroll
           for (int j = 0; j < NPL; ++j) f += ballot_count(kv[j] == thr && lane + 64 * j < t);
@@ -1047,7 +1074,8 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
         ithr = I;
       }
     }
-    // compact the C candidates (lane-major order; the ranking below orders them)
+    // compact the C candidates (lane-major order; the ranking below orders them).  With
+    // an exact threshold (ithr unset) the candidates are the keys >= thr.
     int nsel = 0;
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
@@ -1069,10 +1097,11 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
     }
     const int Cc = min(C, base);
     wave_lds_sync();
+    const double tauZ = static_cast<double>(nk.tau) * Z;
     if (C <= 64) {
-      // rank of lane t's candidate = number of larger candidates (keys are distinct);
-      // the fp64 prefix of the masses is summed in rank order by every lane up to its
-      // own rank, and the first rank reaching tau is read from a ballot
+      // rank of lane t's candidate = number of larger candidates (keys are distinct); the
+      // masses are placed in rank order and summed by an fp64 wave prefix scan, and the
+      // first rank reaching tau Z is read from a ballot
       const unsigned long long x = lane < Cc ? cand[lane] : 0ull;
       const float ex = lane < Cc ? alpha_o[lane] : 0.f;
       int rk = 0;
@@ -1080,13 +1109,8 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
       wave_lds_sync();
       if (lane < Cc) pre_s[rk] = static_cast<double>(ex);
       wave_lds_sync();
-      double incl = 0.0;
-      for (int u = 0; u < Cc; ++u) {
-        const double y = pre_s[u];
-        incl += u <= lane ? y : 0.0;
-      }
-      const double tau = static_cast<double>(a.tau[b]);
-      const unsigned long long hit = __ballot(lane < Cc && incl / Z >= tau);
+      const double incl = wave_incl_scan_f64(lane < Cc ? pre_s[lane] : 0.0);
+      const unsigned long long hit = __ballot(lane < Cc && incl >= tauZ);
       const int K_raw = hit ? __builtin_ctzll(hit) + 1 : (C == nV ? nV : a.k_max + 1);
       K = min(nV, min(a.k_max, max(a.k_min, K_raw)));
       const uint64_t iu = static_cast<uint64_t>(__double_as_longlong(incl));
@@ -1094,9 +1118,10 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
       const uint32_t ihi = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu >> 32), K - 1);
       const double sumI = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(ihi) << 32) | ilo));
       mass = sumI / Z;
+      const double rs = 1.0 / sumI;
       wave_lds_sync();
       if (lane < Cc && rk < K) {
-        alpha_o[rk] = static_cast<float>(static_cast<double>(ex) / sumI);
+        alpha_o[rk] = static_cast<float>(static_cast<double>(ex) * rs);
         idx_o[rk] = static_cast<int>(min(0xFFFFFFFFu - static_cast<uint32_t>(x), static_cast<uint32_t>(M - 1)));
       }
       *mass_o = static_cast<float>(mass);
@@ -1144,10 +1169,9 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
     }
     wave_lds_sync();
     // first rank whose prefix mass reaches tau
-    const double tau = static_cast<double>(a.tau[b]);
     int first = 0x7FFFFFFF;
     for (int t = lane; t < C; t += 64)
-      if (pre_s[t] / Z >= tau) first = min(first, t);
+      if (pre_s[t] >= tauZ) first = min(first, t);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, kWave));
     const int K_raw = first != 0x7FFFFFFF ? first + 1 : (C == nV ? nV : a.k_max + 1);
