@@ -263,8 +263,9 @@ __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
 // Bit pattern of a float as an unsigned key whose integer order is the float order
 // (-0 is mapped onto +0 first so that the two zeros tie, as they compare equal).
 __device__ __forceinline__ uint32_t order_key(float f) {
-  uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  // adding +0 turns -0 into +0 (round to nearest), so both zeros share one key
+  const uint32_t u = __float_as_uint(f + 0.0f);
+  return u ^ (static_cast<uint32_t>(static_cast<int32_t>(u) >> 31) | 0x80000000u);
 }
 
 __device__ __forceinline__ float key_to_float(uint32_t k) {

@@ -1005,22 +1005,27 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
   }
   const int M = nk.M;
   uint32_t lmax = 0;
-  int nV = 0;
 #pragma unroll
-  for (int j = 0; j < NPL; ++j) {
-    lmax = max(lmax, kv[j]);
-    nV += ballot_count((nk.vmask >> j) & 1);
+  for (int j = 0; j < NPL; ++j) lmax = max(lmax, kv[j]);
+  int nV = M;  // without a mask every entry of the request is valid
+  if (a.valid != nullptr) {
+    nV = 0;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) nV += ballot_count((nk.vmask >> j) & 1);
   }
   const uint32_t kmax = __builtin_amdgcn_readfirstlane(wave_max_u32(lmax));
   int K = 0;
   double mass = 0.0;
   if (nV > 0) {
+    // exp(s - smax) as 2^((s - smax) log2 e) on the hardware exp2 (relative error a few
+    // 1e-7 for the entries that carry mass, far inside the score rounding band)
     const float smax = key_to_float(kmax);
+    constexpr float kLog2e = 1.4426950408889634f;
     float ev[NPL];
     double z = 0.0;
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
-      ev[j] = kv[j] != 0u ? expf(key_to_float(kv[j]) - smax) : 0.f;
+      ev[j] = kv[j] != 0u ? __builtin_amdgcn_exp2f((key_to_float(kv[j]) - smax) * kLog2e) : 0.f;
       z += static_cast<double>(ev[j]);
     }
     const double Z = wave_sum_f64(z);
@@ -1041,21 +1046,15 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
         bit = diff != 0u ? 31 - __builtin_clz(diff) : -1;
         thr = diff != 0u ? (kmax & ~((2u << bit) - 1u)) : kmax;
       }
-      bool exact = false;
       for (; bit >= 0; --bit) {
         const uint32_t t = thr | (1u << bit);
         int cnt = 0;
 #pragma unroll
         for (int j = 0; j < NPL; ++j) cnt += ballot_count(kv[j] >= t);
-        if (cnt >= a.k_max) {
-          thr = t;
-          if (cnt == a.k_max) {
-            exact = true;
-            break;
-          }
-        }
+        if (cnt >= a.k_max) thr = t;
+        if (cnt == a.k_max) break;
       }
-      if (!exact) {
+      if (bit < 0) {  // no exact count on the way down
         // thr is the k_max-th largest key itself and more than k_max keys reach it:
         // keep the tied entries with the lowest indices.  I is the largest index bound
         // with #(tied, index < I) < need, so the tied entries with index <= I stay.
@@ -1217,14 +1216,13 @@ __device__ __forceinline__ void gather_rows(const T* __restrict__ vbase, int d_m
     }
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
-    const float w = al[t0 + min(r, nr - 1) * stride];
+    if (r < nr) {  // wave-uniform: padding slots are skipped whole
+      const float w = al[t0 + r * stride];
 #pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const T* v = reinterpret_cast<const T*>(&raw[r][u]);
+      for (int u = 0; u < NCH; ++u) {
+        const T* v = reinterpret_cast<const T*>(&raw[r][u]);
 #pragma unroll
-      for (int x = 0; x < VEC; ++x) {
-        const float f = fmaf(w, Elem<T>::to_f32(v[x]), acc[u][x]);
-        acc[u][x] = r < nr ? f : acc[u][x];
+        for (int x = 0; x < VEC; ++x) acc[u][x] = fmaf(w, Elem<T>::to_f32(v[x]), acc[u][x]);
       }
     }
   }
