@@ -146,7 +146,11 @@ __device__ __forceinline__ void gemm_mainloop_dma(f32x4 (&acc)[C::TM][C::TN],
                                                   int K, int m0, int n0, unsigned char* smem) {
   constexpr int TM = C::TM, TN = C::TN, NST = C::NST;
   constexpr int NI = C::A_DMA + C::B_DMA;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int NH = TM + TN;  // fragments per 32-wide k half
+  const int lane = threadIdx.x & 63;
+  // the wave index is uniform: derived addresses (the direct-to-LDS destinations above
+  // all) stay in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int wm = wave / C::WN, wn = wave % C::WN;
   zero_acc<C>(acc);
 
@@ -181,77 +185,80 @@ __device__ __forceinline__ void gemm_mainloop_dma(f32x4 (&acc)[C::TM][C::TN],
     fa[h] = arow * 128 + (((4 * h + (lane >> 4)) ^ ((arow >> 1) & 7)) << 4);
     fb[h] = brow * 128 + (((4 * h + (lane >> 4)) ^ ((brow >> 1) & 7)) << 4);
   }
-
   const int nk = K / C::BK;
-  auto issue = [&](int kt, int stage) {
-    unsigned char* st = smem + stage * C::STAGE_BYTES;
-    const int k0 = kt * C::BK;
-#pragma unroll
-    for (int j = 0; j < C::A_DMA; ++j)
-      __builtin_amdgcn_global_load_lds(ga[j] + k0, (lds_void_ptr)(st + da[j]), 16, 0, 0);
-#pragma unroll
-    for (int j = 0; j < C::B_DMA; ++j)
-      __builtin_amdgcn_global_load_lds(gb[j] + k0, (lds_void_ptr)(st + db[j]), 16, 0, 0);
+  // fragment r (0 .. NH - 1) of half h of the tile in stage st, in the order the i-major
+  // MFMAs first use them: A0, B0 .. B(TN-1), A1 .. A(TM-1)
+  auto read_frag = [&](const unsigned char* st, int h, int r, bf16x8 (&af)[TM], bf16x8 (&bf)[TN]) {
+    if (r == 0)
+      af[0] = *reinterpret_cast<const bf16x8*>(st + fa[h]);
+    else if (r <= TN)
+      bf[r - 1] = *reinterpret_cast<const bf16x8*>(st + fb[h] + (r - 1) * 16 * 128);
+    else
+      af[r - TN] = *reinterpret_cast<const bf16x8*>(st + fa[h] + (r - TN) * 16 * 128);
   };
-  // Steady state of step kt: wait for tile kt (this thread's loads, then the barrier
-  // for everyone's), read its fragments, run its MFMAs, and load tile kt + NST - 1 into
-  // the stage that tile kt - 1 used.  Loads are issued for every step (past the last
-  // tile the last tile is loaded again into a stage nobody reads), so the number in
-  // flight is constant and the wait is a fixed count, and the body is one basic block
-  // in which the scheduling groups below interleave the LDS reads and the loads with
-  // the MFMAs: the first k half's reads go first, then the second half's reads and the
-  // loads each alternate with one MFMA.  Within a half the reads are ordered
-  // A0, B0..B(TN-1), A1.. as the i-major MFMAs first need them.
-#pragma unroll
-  for (int s = 0; s < NST - 1; ++s) issue(min(s, nk - 1), s);
-  for (int kt = 0; kt < nk; ++kt) {
-    wait_vmcnt<(NST - 2) * NI>();
-    lds_barrier();
+  // load q (0 .. NI - 1) of tile kt into its stage
+  auto issue_one = [&](int kt, int q) {
+    unsigned char* sn = smem + (kt % NST) * C::STAGE_BYTES;
+    const int k0 = kt * C::BK;
+    if (q < C::A_DMA)
+      __builtin_amdgcn_global_load_lds(ga[q] + k0, (lds_void_ptr)(sn + da[q]), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds(gb[q - C::A_DMA] + k0, (lds_void_ptr)(sn + db[q - C::A_DMA]), 16, 0, 0);
+  };
+  // Step kt, with the first k half of tile kt already in registers (set P):
+  //   1. its MFMAs, each followed by one read of the tile's second half and then by one
+  //      load of tile kt + NST - 1 (into the stage tile kt - 1 used);
+  //   2. this wave's reads done, its loads of tile kt + 1 done, then the barrier: tile
+  //      kt + 1 is visible and every wave has finished reading stage kt;
+  //   3. the second half's MFMAs, each followed by one read of tile kt + 1's first half
+  //      (set 1 - P), so that read latency hides behind matrix work.
+  // Loads are issued for every step (past the last tile the last tile is loaded again
+  // into a stage nobody reads), so the wait is a fixed count of this thread's loads
+  // (they retire in issue order).  After the last step the reads of step 3 touch a stage
+  // whose contents are not used.  The compiler barriers keep each access in its slot.
+  bf16x8 af0[2][TM], bf0[2][TN], af1[TM], bf1[TN];
+  auto step = [&](int kt, auto P) {
+    constexpr int p = decltype(P)::value;
     const unsigned char* st = smem + (kt % NST) * C::STAGE_BYTES;
-    const int knext = min(kt + NST - 1, nk - 1), snext = (kt + NST - 1) % NST;
-    bf16x8 af[2][TM], bf[2][TN];
-    // fragment r (0 .. TM + TN - 1) of half h, in the order the i-major MFMAs first use
-    // them: A0, B0 .. B(TN-1), A1 .. A(TM-1)
-    auto read_frag = [&](int h, int r) {
-      if (r == 0)
-        af[h][0] = *reinterpret_cast<const bf16x8*>(st + fa[h]);
-      else if (r <= TN)
-        bf[h][r - 1] = *reinterpret_cast<const bf16x8*>(st + fb[h] + (r - 1) * 16 * 128);
-      else
-        af[h][r - TN] = *reinterpret_cast<const bf16x8*>(st + fa[h] + (r - TN) * 16 * 128);
-    };
-    // load q (0 .. NI - 1) of the tile knext into stage snext
-    auto issue_one = [&](int q) {
-      unsigned char* sn = smem + snext * C::STAGE_BYTES;
-      const int k0 = knext * C::BK;
-      if (q < C::A_DMA)
-        __builtin_amdgcn_global_load_lds(ga[q] + k0, (lds_void_ptr)(sn + da[q]), 16, 0, 0);
-      else
-        __builtin_amdgcn_global_load_lds(gb[q - C::A_DMA] + k0, (lds_void_ptr)(sn + db[q - C::A_DMA]), 16, 0, 0);
-    };
-    // first half's reads; then its MFMAs, each followed by one of the second half's
-    // reads and then by one of the loads of a later tile; the compiler barriers keep
-    // every LDS access and load at its place between the MFMAs
-    constexpr int NH = TM + TN;
-#pragma unroll
-    for (int r = 0; r < NH; ++r) read_frag(0, r);
-    asm volatile("" ::: "memory");
+    const unsigned char* sn = smem + ((kt + 1) % NST) * C::STAGE_BYTES;
+    const int knext = min(kt + NST - 1, nk - 1);
 #pragma unroll
     for (int m = 0; m < TM * TN; ++m) {
-      mfma_bf16_16x16x32_acc(acc[m / TN][m % TN], af[0][m / TN], bf[0][m % TN]);
+      mfma_bf16_16x16x32_acc(acc[m / TN][m % TN], af0[p][m / TN], bf0[p][m % TN]);
       if (m < NH)
-        read_frag(1, m);
+        read_frag(st, 1, m, af1, bf1);
       else if (m - NH < NI)
-        issue_one(m - NH);
+        issue_one(knext, m - NH);
       asm volatile("" ::: "memory");
     }
 #pragma unroll
-    for (int q = TM * TN - NH; q < NI; ++q) issue_one(q);
-    asm volatile("" ::: "memory");
+    for (int q = TM * TN - NH; q < NI; ++q) issue_one(knext, q);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of the stage done
+    wait_vmcnt<(NST - 2) * NI>();
+    lds_barrier();
 #pragma unroll
-    for (int m = 0; m < TM * TN; ++m)
-      mfma_bf16_16x16x32_acc(acc[m / TN][m % TN], af[1][m / TN], bf[1][m % TN]);
+    for (int m = 0; m < TM * TN; ++m) {
+      mfma_bf16_16x16x32_acc(acc[m / TN][m % TN], af1[m / TN], bf1[m % TN]);
+      if (m < NH) read_frag(sn, 0, m, af0[1 - p], bf0[1 - p]);
+      asm volatile("" ::: "memory");
+    }
+  };
+  // prologue: tiles 0 .. NST - 2, each tile's loads together (in issue order)
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s)
+#pragma unroll
+    for (int q = 0; q < NI; ++q) issue_one(min(s, nk - 1), q);
+  wait_vmcnt<(NST - 2) * NI>();
+  lds_barrier();
+#pragma unroll
+  for (int r = 0; r < NH; ++r) read_frag(smem, 0, r, af0[0], bf0[0]);
+  asm volatile("" ::: "memory");
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, std::integral_constant<int, 0>());
+    step(kt + 1, std::integral_constant<int, 1>());
   }
+  if (kt < nk) step(kt, std::integral_constant<int, 0>());
   // the extra loads of the last steps land before the LDS is reused
   wait_vmcnt<0>();
   mfma_results_ready();
