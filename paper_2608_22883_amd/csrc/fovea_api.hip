@@ -276,6 +276,7 @@ ScoreKernel score_kernel_for(int nkc, int kb) {
     case 16: return score_kernel_kb<16>(kb);
     case 20: return score_kernel_kb<20>(kb);
     case 24: return score_kernel_kb<24>(kb);
+    case 64: return score_kernel_kb<64>(kb);
     default: return score_bf16_any_kernel;
   }
 }

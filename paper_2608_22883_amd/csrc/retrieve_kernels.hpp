@@ -882,19 +882,51 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   }
 
   // ---- renormalised gather r = sum_t alpha_t u_{idx_t} (fp32, rank order) ----
-  constexpr int CV = 4;  // columns per thread per pass
-  for (int c = tid * CV; c < a.d_m; c += NT * CV) {
-    float acc[CV] = {0.f, 0.f, 0.f, 0.f};
-    for (int t = 0; t < K; ++t) {
-      const float w = alpha[t];
-      const T* u = a.values + (m0 + sidx[t]) * a.d_m + c;
+  // thread t owns 16-byte chunks t and t + NT of a pass; rows are read in batches of GR
+  // whose loads are all issued before the first multiply-add
+  {
+    constexpr int VEC = Elem<T>::kPer16B;
+    constexpr int GR = 8;
+    const int cpr = a.d_m / VEC;
+    for (int c0 = tid; c0 < cpr; c0 += 2 * NT) {
+      const bool two = c0 + NT < cpr;
+      float acc[2][VEC];
 #pragma unroll
-      for (int j = 0; j < CV; ++j) acc[j] = fmaf(w, Elem<T>::to_f32(u[j]), acc[j]);
-    }
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-    for (int j = 0; j < CV; ++j) {
-      st_f32(a.rT, rbase + c + j, acc[j]);
-      if (a.r_out) a.r_out[rbase + c + j] = acc[j];
+        for (int x = 0; x < VEC; ++x) acc[u][x] = 0.f;
+      for (int t0 = 0; t0 < K; t0 += GR) {
+        const int nr = min(GR, K - t0);
+        u32x4 raw[GR][2];
+#pragma unroll
+        for (int r = 0; r < GR; ++r) {
+          const T* u = a.values + (m0 + sidx[t0 + min(r, nr - 1)]) * a.d_m;
+          raw[r][0] = *reinterpret_cast<const u32x4*>(u + c0 * VEC);
+          raw[r][1] = *reinterpret_cast<const u32x4*>(u + (two ? c0 + NT : c0) * VEC);
+        }
+#pragma unroll
+        for (int r = 0; r < GR; ++r) {
+          if (r < nr) {
+            const float w = alpha[t0 + r];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const T* v = reinterpret_cast<const T*>(&raw[r][u]);
+#pragma unroll
+              for (int x = 0; x < VEC; ++x) acc[u][x] = fmaf(w, Elem<T>::to_f32(v[x]), acc[u][x]);
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        if (u == 1 && !two) break;
+        const int64_t o = rbase + static_cast<int64_t>(c0 + u * NT) * VEC;
+#pragma unroll
+        for (int x = 0; x < VEC; ++x) {
+          st_f32(a.rT, o + x, acc[u][x]);
+          if (a.r_out) a.r_out[o + x] = acc[u][x];
+        }
+      }
     }
   }
   if (a.idx_out)
@@ -1105,17 +1137,25 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
       const float ex = lane < Cc ? alpha_o[lane] : 0.f;
       int rk = 0;
       for (int u = 0; u < Cc; ++u) rk += cand[u] > x ? 1 : 0;
-      wave_lds_sync();
-      if (lane < Cc) pre_s[rk] = static_cast<double>(ex);
-      wave_lds_sync();
-      const double incl = wave_incl_scan_f64(lane < Cc ? pre_s[lane] : 0.0);
-      const unsigned long long hit = __ballot(lane < Cc && incl >= tauZ);
-      const int K_raw = hit ? __builtin_ctzll(hit) + 1 : (C == nV ? nV : a.k_max + 1);
-      K = min(nV, min(a.k_max, max(a.k_min, K_raw)));
-      const uint64_t iu = static_cast<uint64_t>(__double_as_longlong(incl));
-      const uint32_t ilo = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu), K - 1);
-      const uint32_t ihi = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu >> 32), K - 1);
-      const double sumI = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(ihi) << 32) | ilo));
+      double sumI;
+      if (a.k_min == a.k_max) {
+        // fixed cardinality: K = min(|V|, k_max) = C, every candidate is selected, and
+        // only the total of their masses is needed (no prefix, no tau search)
+        K = Cc;
+        sumI = wave_sum_f64(lane < Cc ? static_cast<double>(ex) : 0.0);
+      } else {
+        wave_lds_sync();
+        if (lane < Cc) pre_s[rk] = static_cast<double>(ex);
+        wave_lds_sync();
+        const double incl = wave_incl_scan_f64(lane < Cc ? pre_s[lane] : 0.0);
+        const unsigned long long hit = __ballot(lane < Cc && incl >= tauZ);
+        const int K_raw = hit ? __builtin_ctzll(hit) + 1 : (C == nV ? nV : a.k_max + 1);
+        K = min(nV, min(a.k_max, max(a.k_min, K_raw)));
+        const uint64_t iu = static_cast<uint64_t>(__double_as_longlong(incl));
+        const uint32_t ilo = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu), K - 1);
+        const uint32_t ihi = __builtin_amdgcn_readlane(static_cast<uint32_t>(iu >> 32), K - 1);
+        sumI = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(ihi) << 32) | ilo));
+      }
       mass = sumI / Z;
       const double rs = 1.0 / sumI;
       wave_lds_sync();

@@ -87,6 +87,20 @@ WORKLOADS: dict[str, Workload] = {
         name="stress_video", dtype="bf16", B=8, T=64, M=16384, d=5120, d_m=1280, k_max=256,
         tau=0.9, seed=20260004, key_scale_split=(8.0, 2000.0), frames=16,
         description="high-res / video stress: B=8, M=16384 (16 frames x 1024), d=5120, d_m=1280"),
+    # the paper's own cardinality settings (Method: tau = 0.8, K_min = 32, K_max = 256,
+    # key/value width equal to the hidden size) and its fixed-K ablation (K_r = 16)
+    "paper_llava": Workload(
+        name="paper_llava", dtype="bf16", B=1, T=60, M=576, d=4096, d_m=4096, k_min=32,
+        k_max=256, tau=0.8, seed=20260005, key_scale=(80.0, 80.0), boost_frac=0.10,
+        boost=2.0,
+        description="paper preset on the LLaVA-1.5-7B shape: tau=0.8, K_min=32, K_max=256, "
+                    "d_m=d=4096, B=1, T=60, M=576"),
+    "fixed16_b32": Workload(
+        name="fixed16_b32", dtype="bf16", B=32, T=60, M=576, d=4096, d_m=1024, k_min=16,
+        k_max=16, tau=0.6, tau_hi=0.95, seed=20260006, key_scale=(35.0, 250.0),
+        boost_frac=0.10, boost=1.5,
+        description="fixed cardinality K=16 on the batched shape: B=32, T=60, M=576, "
+                    "d=4096, d_m=1024"),
 }
 
 

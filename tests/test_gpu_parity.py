@@ -49,7 +49,8 @@ def _run(lib, case, W=None, fv=None):
 
 @pytest.mark.parametrize("name,affine", [
     ("tiny_f32", "unit"), ("tiny_f32", "random"), ("llava_b1", "unit"), ("llava_b1", "random"),
-    ("batched_b32", "unit"), ("qwen_ragged", "unit"), ("stress_video", "unit")])
+    ("batched_b32", "unit"), ("qwen_ragged", "unit"), ("stress_video", "unit"),
+    ("paper_llava", "unit"), ("fixed16_b32", "unit")])
 def test_workload_parity(lib, name, affine):
     wl = WORKLOADS[name]
     case = make_case(wl, affine=affine)

@@ -415,7 +415,8 @@ def test_gain_fold_is_exact_for_exact_products():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["tiny_f32", "llava_b1", "batched_b32", "qwen_ragged"])
+@pytest.mark.parametrize("name", ["tiny_f32", "llava_b1", "batched_b32", "qwen_ragged",
+                                  "paper_llava", "fixed16_b32"])
 def test_workload_cardinality_mix(name):
     wl = WORKLOADS[name]
     c = make_case(wl)
@@ -432,6 +433,11 @@ def test_workload_cardinality_mix(name):
         Ms = np.diff(c.mem_off)
         assert Ms.min() >= 256 and Ms.max() <= 4096 and Ms.max() - Ms.min() > 1500
         assert K.max() <= wl.k_max and K.min() >= 1
+    elif name == "paper_llava":
+        # K_min = 32 holds every set at 32 or more; the mass rule raises some above it
+        assert K.min() >= wl.k_min and K.max() <= wl.k_max and (K > wl.k_min).any()
+    elif name == "fixed16_b32":
+        assert (K == 16).all()
 
 
 @pytest.mark.slow
