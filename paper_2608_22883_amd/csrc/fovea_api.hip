@@ -384,12 +384,17 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
 #undef FOVEA_SEL
 #undef FOVEA_SEL_C
     } else {
-      const size_t sel_smem = static_cast<size_t>(a.m_max) * 4;
-      if (sel_smem > 0)
-        FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
-                                      hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      static_cast<int>(sel_smem)));
-      hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n), dim3(256), sel_smem, s, sa);
+      // the order keys, later reused for the gather's partial sums (3 x 64 lanes x VEC)
+      const size_t sel_smem = std::max(static_cast<size_t>(a.m_max) * 4,
+                                       static_cast<size_t>(3 * 64 * VEC * 4));
+      FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    static_cast<int>(sel_smem)));
+      // few nodes: each node's row is also split into column slices over several blocks
+      // (each repeats the selection) so that the gathers run on more compute units
+      const int cpr64 = (D.d_m / VEC + 63) / 64;
+      const int slices = std::max(1, std::min(cpr64, 512 / std::max(a.n, 1)));
+      hipLaunchKernelGGL(select_gather_kernel<T>, dim3(a.n, slices), dim3(256), sel_smem, s, sa);
     }
   }
   // 5. correction layer 1: the r half, plus P, bias and SiLU (+ gate logit partials)

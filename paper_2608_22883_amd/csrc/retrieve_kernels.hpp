@@ -881,54 +881,64 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
     __syncthreads();
   }
 
-  // ---- renormalised gather r = sum_t alpha_t u_{idx_t} (fp32, rank order) ----
-  // thread t owns 16-byte chunks t and t + NT of a pass; rows are read in batches of GR
-  // whose loads are all issued before the first multiply-add
+  // ---- renormalised gather r = sum_t alpha_t u_{idx_t} ----
+  // This block covers the 16-byte chunks [c_lo, c_hi) of the row (its column slice);
+  // lane l takes chunk c_lo + l + 64 j in pass j, wave w the ranks w, w + 4, .. in
+  // batches of GR rows whose loads all issue before the first multiply-add; the four
+  // partial sums are added by wave 0 in a fixed order through LDS.
   {
     constexpr int VEC = Elem<T>::kPer16B;
     constexpr int GR = 8;
     const int cpr = a.d_m / VEC;
-    for (int c0 = tid; c0 < cpr; c0 += 2 * NT) {
-      const bool two = c0 + NT < cpr;
-      float acc[2][VEC];
+    const int ns = gridDim.y;
+    const int c_lo = static_cast<int>(static_cast<int64_t>(cpr) * blockIdx.y / ns);
+    const int c_hi = static_cast<int>(static_cast<int64_t>(cpr) * (blockIdx.y + 1) / ns);
+    const int lane = tid & 63, w = tid >> 6;
+    const int mine = K > w ? (K - w + 3) / 4 : 0;
+    float* red = reinterpret_cast<float*>(skey);  // the keys are no longer needed
+    for (int cb = c_lo; cb < c_hi; cb += 64) {
+      const int c = min(cb + lane, c_hi - 1);
+      float acc[VEC];
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int x = 0; x < VEC; ++x) acc[u][x] = 0.f;
-      for (int t0 = 0; t0 < K; t0 += GR) {
-        const int nr = min(GR, K - t0);
-        u32x4 raw[GR][2];
+      for (int x = 0; x < VEC; ++x) acc[x] = 0.f;
+      for (int q0 = 0; q0 < mine; q0 += GR) {
+        const int nr = min(GR, mine - q0);
+        u32x4 raw[GR];
 #pragma unroll
         for (int r = 0; r < GR; ++r) {
-          const T* u = a.values + (m0 + sidx[t0 + min(r, nr - 1)]) * a.d_m;
-          raw[r][0] = *reinterpret_cast<const u32x4*>(u + c0 * VEC);
-          raw[r][1] = *reinterpret_cast<const u32x4*>(u + (two ? c0 + NT : c0) * VEC);
+          const int t = w + 4 * (q0 + min(r, nr - 1));
+          raw[r] = *reinterpret_cast<const u32x4*>(a.values + (m0 + sidx[t]) * a.d_m + c * VEC);
         }
 #pragma unroll
         for (int r = 0; r < GR; ++r) {
           if (r < nr) {
-            const float w = alpha[t0 + r];
+            const float wt = alpha[w + 4 * (q0 + r)];
+            const T* v = reinterpret_cast<const T*>(&raw[r]);
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const T* v = reinterpret_cast<const T*>(&raw[r][u]);
-#pragma unroll
-              for (int x = 0; x < VEC; ++x) acc[u][x] = fmaf(w, Elem<T>::to_f32(v[x]), acc[u][x]);
-            }
+            for (int x = 0; x < VEC; ++x) acc[x] = fmaf(wt, Elem<T>::to_f32(v[x]), acc[x]);
           }
         }
       }
+      if (w > 0)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        if (u == 1 && !two) break;
-        const int64_t o = rbase + static_cast<int64_t>(c0 + u * NT) * VEC;
+        for (int x = 0; x < VEC; ++x) red[((w - 1) * 64 + lane) * VEC + x] = acc[x];
+      __syncthreads();
+      if (w == 0 && cb + lane < c_hi) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+#pragma unroll
+          for (int x = 0; x < VEC; ++x) acc[x] += red[(q * 64 + lane) * VEC + x];
+        const int64_t o = rbase + static_cast<int64_t>(c) * VEC;
 #pragma unroll
         for (int x = 0; x < VEC; ++x) {
-          st_f32(a.rT, o + x, acc[u][x]);
-          if (a.r_out) a.r_out[o + x] = acc[u][x];
+          st_f32(a.rT, o + x, acc[x]);
+          if (a.r_out) a.r_out[o + x] = acc[x];
         }
       }
+      __syncthreads();
     }
   }
+  if (blockIdx.y != 0) return;  // one block of the node writes the selection outputs
   if (a.idx_out)
     for (int t = tid; t < a.k_max; t += NT)
       a.idx_out[static_cast<int64_t>(n) * a.k_max + t] = t < K ? sidx[t] : -1;
