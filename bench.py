@@ -14,6 +14,11 @@ HIP events after a device synchronisation.  A second, profiled pass brackets eve
 kernel with HIP events for the per-kernel roofline.  The fp64 oracle is timed on the
 host cores on a bounded sample as the CPU baseline.
 
+--lm-head vicuna7b|qwen2_5_7b extends every step by the drafter's LM head over the
+corrected states and the top-K_c (--kc, default 6) candidate extraction
+(fovea_lm_topk), with a synthetic head of that vocabulary; the CPU baseline is then
+skipped.
+
 Prints one JSON line.
 """
 
@@ -48,6 +53,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=6, help="input copies rotated in the timed loop")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lm-head", default=None, choices=["vicuna7b", "qwen2_5_7b"],
+                    help="extend the step by the drafter's LM head and top-K_c candidates")
+    ap.add_argument("--kc", type=int, default=6, help="candidates per node with --lm-head")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
     return ap.parse_args()
@@ -96,7 +104,7 @@ def copy_calibration():
     print(json.dumps(dict(copy_bytes_read=n, copy_bytes_written=n, dispatches=10)), flush=True)
 
 
-def kernel_model(wl, case, union_rows, k_sum):
+def kernel_model(wl, case, union_rows, k_sum, lm=None, kc=0):
     """Algorithmic bytes and flops per launch of each kernel (storage dtype es)."""
     import numpy as np
 
@@ -117,6 +125,11 @@ def kernel_model(wl, case, union_rows, k_sum):
                       flops=2 * n * d_m * 2 * d_c)
     k["corr2"] = dict(bytes=n * d_c * es + d * d_c * es + 2 * n * d * es, flops=2 * n * d_c * d)
     k["rms"] = dict(bytes=2 * n * d * es, flops=3 * n * d)
+    if lm is not None:
+        cand = n * ((lm["vocab"] + 127) // 128) * kc * 8
+        k["lm_head"] = dict(bytes=lm["vocab"] * d * es + n * d * es + cand,
+                            flops=2 * n * d * lm["vocab"])
+        k["lm_merge"] = dict(bytes=cand + n * kc * 8, flops=0)
     # the retrieval as one operation: every key, q, the selected value rows, r
     retrieval = dict(bytes=n_mem * d_m * es + n * d_m * 4 + union_rows * d_m * es + n * d_m * es,
                      flops=2 * pairs * d_m)
@@ -192,6 +205,22 @@ def main():
                           h=base["h"].clone()) for _ in range(args.copies - 1)]
     per_set = sum(base[k].numel() * base[k].element_size() for k in ("keys", "values", "h"))
     out = fv.alloc_outputs(case.n_nodes, case.k_max, wl.d, wl.d_m)
+    lm = None
+    if args.lm_head:
+        from synth import LM_HEADS, make_lm_case
+
+        lm = dict(LM_HEADS[args.lm_head], name=args.lm_head)
+        if lm["d"] != wl.d:
+            log(f"[bench] {args.lm_head} has d={lm['d']}, the workload d={wl.d}")
+            sys.exit(2)
+        _, W_lm = make_lm_case(1, wl.d, lm["vocab"], wl.dtype, seed=wl.seed + 31)
+        W_lm = dev_t(W_lm)
+        lm_idx = torch.empty(case.n_nodes, args.kc, dtype=torch.int32, device=dev)
+
+    def step(i, debug=False):
+        fv.retrieve_fuse(sets[i % len(sets)], out, debug=debug)
+        if lm is not None:
+            fv.lm_topk(out.h_out, W_lm, args.kc, idx=lm_idx, want_logits=False)
 
     # one debug run: selected sets (for the algorithmic gather bytes) and a sanity check
     fv.retrieve_fuse(base, out, debug=True)
@@ -207,13 +236,13 @@ def main():
 
     # whole-step timing
     for i in range(args.warmup):
-        fv.retrieve_fuse(sets[i % len(sets)], out, debug=False)
+        step(i)
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(args.steps):
-        fv.retrieve_fuse(sets[i % len(sets)], out, debug=False)
+        step(i)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
@@ -222,20 +251,21 @@ def main():
     # per-kernel timing (events around each kernel, on the library's stream)
     fovea_profile(fv.ctx, True)
     for i in range(args.steps):
-        fv.retrieve_fuse(sets[i % len(sets)], out, debug=False)
+        step(i)
     torch.cuda.synchronize()
     prof = fovea_profile_read(fv.ctx)
     fovea_profile(fv.ctx, False)
 
-    kmodel, retrieval = kernel_model(wl, case, union_rows, int(K.sum()))
+    kmodel, retrieval = kernel_model(wl, case, union_rows, int(K.sum()), lm, args.kc)
+    peak_fl = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
     kernels = []
     for name, (tot, cnt) in prof.items():
         avg_ms = tot / cnt
         m = kmodel.get(name, dict(bytes=0, flops=0))
         gbs = m["bytes"] / (avg_ms * 1e-3) / 1e9
         tfl = m["flops"] / (avg_ms * 1e-3) / 1e12
-        peak_fl = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
-        mfma = name in ("hq", "corr1", "corr2")
+        mfma = name in ("hq", "corr1", "corr2") or (
+            name == "lm_head" and m["flops"] / m["bytes"] > peak_fl / PEAK_HBM_GBS * 1e3)
         kernels.append(dict(
             name=name, avg_us=round(avg_ms * 1e3, 2), launches=cnt, alg_bytes=m["bytes"],
             alg_flops=m["flops"], GBs=round(gbs, 1), TFLOPs=round(tfl, 2),
@@ -255,15 +285,21 @@ def main():
     ret_us = sum(k["avg_us"] for k in kernels if k["name"] in ("score", "select_gather"))
     ret_gbs = retrieval["bytes"] / (ret_us * 1e-6) / 1e9 if ret_us else 0.0
 
+    metric = "draft states/sec for retrieve+fuse (M=576, d=4096); % of peak HBM GB/s"
+    if lm is not None:
+        metric = (f"draft states/sec for retrieve+fuse + LM head ({lm['name']}, vocab "
+                  f"{lm['vocab']}) top-{args.kc} candidates")
     line = dict(
-        metric="draft states/sec for retrieve+fuse (M=576, d=4096); % of peak HBM GB/s",
+        metric=metric,
         value=round(case.n_nodes / (ms * 1e-3), 1), unit="states/s", n_gpus=1,
         steps=args.steps, warmup=args.warmup, ms_per_step=round(ms, 5), higher_is_better=True,
         scaling="weak", vs_baseline=None, dtype=wl.dtype, data="synthetic",
         config=dict(workload=wl.name, description=wl.description, B=wl.B, T=wl.T, M=wl.M,
                     d=wl.d, d_m=wl.d_m, d_c=wl.d_c, k_max=wl.k_max,
                     states_per_step=case.n_nodes, input_copies=len(sets),
-                    rotated_bytes=per_set * len(sets)),
+                    rotated_bytes=per_set * len(sets),
+                    **({} if lm is None else dict(lm_head=lm["name"], vocab=lm["vocab"],
+                                                  kc=args.kc))),
         roofline=roof,
         retrieval=dict(kernels=["score", "select_gather"], us=round(ret_us, 2),
                        alg_bytes=retrieval["bytes"], GBs=round(ret_gbs, 1),
@@ -272,7 +308,7 @@ def main():
         K=dict(min=int(K.min()), median=float(np.median(K)), max=int(K.max()),
                union_value_rows=int(union_rows)),
     )
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and lm is None:
         log("[bench] timing the oracle on the host ...")
         line["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
     fv.close()

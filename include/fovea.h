@@ -160,13 +160,41 @@ fovea_status fovea_retrieve_fuse(fovea_ctx* ctx, int32_t B, const int64_t* mem_o
                                  float* r_out, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* Limits of the candidate extraction below. */
+#define FOVEA_LM_MAX_K 16             /* candidates per row */
+#define FOVEA_LM_MAX_VOCAB (1 << 24)  /* vocabulary size */
+#define FOVEA_LM_MAX_ROWS (1 << 20)   /* rows per call */
+
+/* Bytes of workspace fovea_lm_topk needs for these sizes (0 on bad arguments). */
+size_t fovea_lm_topk_workspace(const fovea_ctx* ctx, int32_t n_rows, int32_t vocab, int32_t k);
+
+/* Draft candidates of every corrected state (Eq. hidden_correction's z_n = W_LM h_hat_n
+ * and Algorithm 1's expansion step, which adds each node's K_c most likely tokens to the
+ * draft tree; K_c = 6 in the experiments):
+ *   z_n = W_LM h[n]  over the whole vocabulary, then the k largest entries of z_n.
+ *   h        [n_rows, d] storage dtype, device (typically fovea_retrieve_fuse's h_out).
+ *   W_LM     [vocab, d] storage dtype, device: the language-model head, [out, in].  Read
+ *            in place, not copied; the caller keeps it alive until the call has run.
+ *   k        1 <= k <= min(vocab, FOVEA_LM_MAX_K).
+ * Outputs (device):
+ *   idx_out   [n_rows, k] int32: token ids by descending logit, equal logits by
+ *             ascending id.  A NaN logit is never chosen; a slot with nothing left to
+ *             choose (every remaining logit NaN) holds -1.
+ *   logit_out [n_rows, k] float32 or NULL: the chosen logits (-inf where idx is -1).
+ * The logits are accumulated in fp32 and never written to memory.
+ * workspace: device memory of at least fovea_lm_topk_workspace(...) bytes, 256-byte
+ * aligned, clobbered.  Outputs must not overlap the workspace or each other. */
+fovea_status fovea_lm_topk(fovea_ctx* ctx, int32_t n_rows, const void* h, const void* W_LM,
+                           int32_t vocab, int32_t k, int32_t* idx_out, float* logit_out,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Synchronise `stream`, read and clear the context's sticky device-data error bits.
  * Returns FOVEA_ERR_DATA if any bit was set (the bits go to *bits if non-NULL),
  * FOVEA_ERR_DEVICE on a HIP error, else FOVEA_OK. */
 fovea_status fovea_last_error(fovea_ctx* ctx, hipStream_t stream, uint32_t* bits);
 
 /* Diagnostics: per-kernel timing with HIP events.  While enabled, every kernel that
- * fovea_retrieve_fuse or fovea_build_memory launches is bracketed by two HIP events on
+ * fovea_retrieve_fuse, fovea_build_memory or fovea_lm_topk launches is bracketed by two HIP events on
  * the call's stream (this adds event packets between the kernels, so time whole calls
  * with profiling off).  fovea_profile_read waits for the recorded events, writes up to
  * max_kernels entries (kernel name, summed milliseconds, launch count; names are

@@ -23,6 +23,9 @@ from .fovea_ref import (  # noqa: F401
     fold_gain,
     fuse,
     layer_norm,
+    lm_logits,
+    lm_topk,
+    lm_topk_from_logits,
     projected_layer_norm,
     query,
     readout,

@@ -16,6 +16,9 @@ Sources (paper section / equation):
     nets two biased linear layers with a 512-wide SiLU hidden layer; the scalar gate is
     broadcast over the hidden size; h_hat = RMSNorm(h_n + g_n c_n) (Eq. hidden_correction).
   * Algorithm 1 orders the per-node steps the same way.
+  * Eq. hidden_correction's z_n = W_LM h_hat_n and Algorithm 1's tree expansion, which
+    adds each node's K_c highest-scoring tokens (K_c = 6 in the experimental setup):
+    ``lm_topk``.
 
 Readings where the paper is silent (each one is listed with its reason in the design notes):
   * ties in the descending rank are broken by ascending memory index;
@@ -25,13 +28,17 @@ Readings where the paper is silent (each one is listed with its reason in the de
   * |V| = 0 gives K = 0 and a zero readout; the correction is still applied;
   * LayerNorm is affine with biased variance; RMSNorm has a weight (optional: None
     returns h + g c unnormalised, the reading used for the "gate = 0 returns h" check);
-  * the concatenation is [h; r] with h first; W_Q, W_K, W_U have no bias.
+  * the concatenation is [h; r] with h first; W_Q, W_K, W_U have no bias;
+  * the K_c candidates of a node are its K_c largest logits, equal logits by ascending
+    token id; a NaN logit is never a candidate, and a slot left without one holds -1.
 
 Parity pins (tests/test_oracle.py): brute-force subset enumeration, closed forms for
 uniform and geometric score profiles, the dense special case against PyTorch's
 scaled-dot-product attention, LayerNorm/RMSNorm/linear against torch.nn.functional,
 the peaked case (K = 1, readout equals the value row exactly), gate = 0 and gate = 1
-special cases, invariants (mass, clamps, permutation equivariance, masking).  The
+special cases, invariants (mass, clamps, permutation equivariance, masking); for
+``lm_topk``, pure-Python brute force (dot products and repeated arg-max scans),
+exact ties from duplicated head rows, and the k = vocab case as a full sort.  The
 correction MLPs at random weights have no independent numeric fixture in the paper:
 they are pinned through the gate special cases and the torch cross-check of each
 linear layer, not through a printed example.
@@ -57,6 +64,9 @@ __all__ = [
     "correction",
     "fuse",
     "retrieve_fuse",
+    "lm_logits",
+    "lm_topk",
+    "lm_topk_from_logits",
 ]
 
 
@@ -271,3 +281,31 @@ def retrieve_fuse(W, mem_off, keys, values, valid, node_off, h, depth, tau, k_mi
                       W["w_g2"], W["b_g2"])
     h_out = fuse(h, g, c, W.get("rms_w"), W["rms_eps"])
     return dict(h_out=h_out, K=K, idx=idx, gate=g, mass=mass, r=r, q=q, records=records)
+
+
+def lm_logits(h, W_LM):
+    """z_n = W_LM h_n for every row (Eq. hidden_correction), in fp64."""
+    return np.asarray(h, np.float64) @ np.asarray(W_LM, np.float64).T
+
+
+def lm_topk(h, W_LM, k):
+    """The k draft candidates of every row (Algorithm 1, tree expansion): token ids of
+    the k largest logits, descending, equal logits by ascending id; NaN logits are
+    skipped and an unfilled slot holds id -1 and logit -inf.  Returns (idx, logits)."""
+    return lm_topk_from_logits(lm_logits(h, W_LM), k)
+
+
+def lm_topk_from_logits(z, k):
+    """The candidate rule of ``lm_topk`` applied to given logits [n, vocab]."""
+    z = np.asarray(z, np.float64)
+    n, vocab = z.shape
+    idx = np.full((n, k), -1, np.int64)
+    val = np.full((n, k), -np.inf)
+    ids = np.arange(vocab)
+    for r in range(n):
+        ok = ~np.isnan(z[r])
+        # lexsort: last key is primary -> by -z, then by id
+        order = ids[ok][np.lexsort((ids[ok], -z[r][ok]))][:k]
+        idx[r, : order.size] = order
+        val[r, : order.size] = z[r][order]
+    return idx, val

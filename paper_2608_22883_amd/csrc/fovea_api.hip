@@ -10,9 +10,15 @@
 
 #include "fovea.h"
 #include "correct_kernels.hpp"
+#include "lm_kernels.hpp"
 #include "retrieve_kernels.hpp"
 
 using namespace fovea;
+
+static_assert(FOVEA_MAX_M == kMaxM && FOVEA_MAX_KMAX == kMaxKmax, "header limits");
+static_assert(FOVEA_LM_MAX_K == kLmMaxK && FOVEA_LM_MAX_VOCAB == kLmMaxVocab &&
+                  FOVEA_LM_MAX_ROWS == kLmMaxRows,
+              "header limits");
 
 struct fovea_ctx {
   fovea_dims dims;
@@ -103,9 +109,13 @@ bool dims_supported(const fovea_dims* d) {
     if ((call) != hipSuccess) return FOVEA_ERR_DEVICE;    \
   } while (0)
 
-enum KernelSlot { kRowStats, kHq, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kNumSlots };
-const char* const kSlotNames[kNumSlots] = {"row_stats", "hq", "score", "select_gather",
-                                           "corr1", "corr2", "rms", "mem_row_stats", "mem_proj"};
+enum KernelSlot {
+  kRowStats, kHq, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kLmHead, kLmMerge,
+  kNumSlots
+};
+const char* const kSlotNames[kNumSlots] = {"row_stats", "hq",       "score",         "select_gather",
+                                           "corr1",     "corr2",    "rms",           "mem_row_stats",
+                                           "mem_proj",  "lm_head",  "lm_merge"};
 
 hipEvent_t prof_event(fovea_ctx* c) {
   if (!c->prof_pool.empty()) {
@@ -427,6 +437,42 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   return FOVEA_OK;
 }
 
+size_t lm_cand_bytes(int n, int vocab, int k) {
+  const size_t cb = (static_cast<size_t>(vocab) + 127) / 128;
+  return align_up(static_cast<size_t>(n) * cb * k * sizeof(LmCand));
+}
+
+template <typename T, int BM>
+void launch_lm(int n, const T* h, int d, const T* W, int vocab, int k, LmCand* cand,
+               hipStream_t s) {
+  const LmMap m = make_lm_map((n + BM - 1) / BM, (vocab + 127) / 128);
+  hipLaunchKernelGGL((lm_kernel<T, BM>), dim3(lm_grid(m)), dim3(256), 0, s, m, n, h, d, W, vocab,
+                     k, cand);
+}
+
+template <typename T>
+fovea_status run_lm_topk(fovea_ctx* c, int n, const void* h, const void* W, int vocab, int k,
+                         int32_t* idx, float* logit, LmCand* cand, hipStream_t s) {
+  const int d = c->dims.d;
+  {
+    ProfScope ps(c, kLmHead, s);
+    if (n <= 64)
+      launch_lm<T, 64>(n, static_cast<const T*>(h), d, static_cast<const T*>(W), vocab, k, cand, s);
+    else
+      launch_lm<T, 128>(n, static_cast<const T*>(h), d, static_cast<const T*>(W), vocab, k, cand, s);
+  }
+  {
+    const int n_cand = (vocab + 127) / 128 * k;
+    ProfScope ps(c, kLmMerge, s);
+    if (k <= 8)
+      hipLaunchKernelGGL(lm_merge_kernel<8>, dim3(n), dim3(256), 0, s, n_cand, k, cand, idx, logit);
+    else
+      hipLaunchKernelGGL(lm_merge_kernel<kLmMaxK>, dim3(n), dim3(256), 0, s, n_cand, k, cand, idx,
+                         logit);
+  }
+  return hipGetLastError() == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+}
+
 }  // namespace
 
 extern "C" {
@@ -665,6 +711,37 @@ int32_t fovea_profile_read(fovea_ctx* c, int32_t max_kernels, const char** names
     ++w;
   }
   return w;
+}
+
+size_t fovea_lm_topk_workspace(const fovea_ctx* c, int32_t n_rows, int32_t vocab, int32_t k) {
+  if (c == nullptr || n_rows < 0 || k < 1 || k > kLmMaxK || vocab < k || vocab > kLmMaxVocab ||
+      n_rows > kLmMaxRows)
+    return 0;
+  return lm_cand_bytes(n_rows, vocab, k);
+}
+
+fovea_status fovea_lm_topk(fovea_ctx* c, int32_t n_rows, const void* h, const void* W_LM,
+                           int32_t vocab, int32_t k, int32_t* idx_out, float* logit_out,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (c == nullptr || n_rows < 0 || k < 1 || vocab < k) return FOVEA_ERR_INVALID_ARG;
+  if (k > kLmMaxK || vocab > kLmMaxVocab || n_rows > kLmMaxRows) return FOVEA_ERR_UNSUPPORTED;
+  if (n_rows == 0) return FOVEA_OK;
+  if (h == nullptr || W_LM == nullptr || idx_out == nullptr || workspace == nullptr)
+    return FOVEA_ERR_INVALID_ARG;
+  if (!aligned16(h) || !aligned16(W_LM)) return FOVEA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return FOVEA_ERR_WORKSPACE;
+  const size_t need = lm_cand_bytes(n_rows, vocab, k);
+  if (workspace_bytes < need) return FOVEA_ERR_WORKSPACE;
+  const size_t ni = static_cast<size_t>(n_rows) * k * 4;
+  if (overlaps(idx_out, ni, workspace, need) || overlaps(logit_out, ni, workspace, need) ||
+      overlaps(idx_out, ni, logit_out, ni))
+    return FOVEA_ERR_INVALID_ARG;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
+  LmCand* cand = static_cast<LmCand*>(workspace);
+  return c->bf16 ? run_lm_topk<bf16_t>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream)
+                 : run_lm_topk<float>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream);
 }
 
 }  // extern "C"

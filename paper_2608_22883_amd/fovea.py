@@ -32,11 +32,15 @@ FOVEA_DATA_BAD_TAU = 0x8
 
 FOVEA_MAX_M = 16384
 FOVEA_MAX_KMAX = 1024
+FOVEA_LM_MAX_K = 16
+FOVEA_LM_MAX_VOCAB = 1 << 24
+FOVEA_LM_MAX_ROWS = 1 << 20
 
 EXPORTED = [
     "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
     "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
-    "fovea_last_error", "fovea_profile", "fovea_profile_read",
+    "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
+    "fovea_lm_topk",
 ]
 
 
@@ -89,6 +93,10 @@ def _load() -> ctypes.CDLL:
     lib.fovea_profile_read.restype = i32
     lib.fovea_profile_read.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_char_p),
                                        ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
+    lib.fovea_lm_topk_workspace.restype = sz
+    lib.fovea_lm_topk_workspace.argtypes = [vp, i32, i32, i32]
+    lib.fovea_lm_topk.restype = ctypes.c_int
+    lib.fovea_lm_topk.argtypes = [vp, i32, vp, vp, i32, i32, vp, vp, vp, sz, vp]
     return lib
 
 
@@ -179,6 +187,21 @@ def fovea_retrieve_fuse(ctx: int, B: int, mem_off, n_mem_total: int, m_max: int,
     _check(st, "fovea_retrieve_fuse")
 
 
+def fovea_lm_topk_workspace(ctx: int, n_rows: int, vocab: int, k: int) -> int:
+    return lib.fovea_lm_topk_workspace(ctx, n_rows, vocab, k)
+
+
+def fovea_lm_topk(ctx: int, n_rows: int, h, W_LM, vocab: int, k: int, idx_out, logit_out=None,
+                  workspace=None, stream=None) -> None:
+    """Same arguments as the C entry point; tensors stand for device pointers."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.fovea_lm_topk(
+        ctx, n_rows, _ptr(h, None, "h"), _ptr(W_LM, h.dtype, "W_LM"), vocab, k,
+        _ptr(idx_out, torch.int32, "idx_out"), _ptr(logit_out, torch.float32, "logit_out"),
+        _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+    _check(st, "fovea_lm_topk")
+
+
 def fovea_last_error(ctx: int, stream=None) -> tuple[int, int]:
     bits = ctypes.c_uint32(0)
     st = lib.fovea_last_error(ctx, _stream(stream), ctypes.byref(bits))
@@ -231,6 +254,7 @@ class Fovea:
             self.params[n] = torch.as_tensor(v).to(device=self.device, dtype=self.dtype).contiguous()
         self.ctx = fovea_create(self.dims, self.params, float(weights["b_g2"]), stream)
         self.workspace = None
+        self.lm_workspace = None
 
     def close(self):
         if getattr(self, "ctx", None):
@@ -277,3 +301,17 @@ class Fovea:
             out.k if debug else None, out.idx if debug else None, out.gate if debug else None,
             out.mass if debug else None, out.r if debug else None, ws, stream)
         return out
+
+    def lm_topk(self, h: torch.Tensor, W_LM: torch.Tensor, k: int, idx: torch.Tensor | None = None,
+                logit: torch.Tensor | None = None, want_logits: bool = True, stream=None):
+        """Top-k token ids (and logits) of W_LM h for every row of h ([n, d])."""
+        n, vocab = h.shape[0], W_LM.shape[0]
+        if idx is None:
+            idx = torch.empty(n, k, dtype=torch.int32, device=self.device)
+        if logit is None and want_logits:
+            logit = torch.empty(n, k, dtype=torch.float32, device=self.device)
+        need = fovea_lm_topk_workspace(self.ctx, n, vocab, k)
+        if self.lm_workspace is None or self.lm_workspace.numel() < need:
+            self.lm_workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        fovea_lm_topk(self.ctx, n, h, W_LM, vocab, k, idx, logit, self.lm_workspace, stream)
+        return idx, logit

@@ -271,3 +271,21 @@ def make_memory_case(wl: Workload, n_rows: int, seed: int | None = None, affine:
     W = make_weights(wl, seed + 7919, affine) if weights is None else weights
     V = _normal(rng, (n_rows, wl.d), 1.0, wl.dtype)
     return V, W
+
+
+# Language-model heads of the drafters the paper evaluates: LLaVA-NeXT-7B's Vicuna head
+# (vocabulary 32000, hidden 4096) and Qwen2.5-VL-7B's (vocabulary 152064, hidden 3584).
+LM_HEADS = {
+    "vicuna7b": dict(vocab=32000, d=4096),
+    "qwen2_5_7b": dict(vocab=152064, d=3584),
+}
+
+
+def make_lm_case(n: int, d: int, vocab: int, dtype: str, seed: int):
+    """Corrected states h ~ N(0, 1) (unit RMS, as after the RMSNorm) and a head
+    W_LM ~ N(0, 1/d), so that logits are of unit scale.  Both rounded once to the
+    storage dtype; returned as float64."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    h = _normal(rng, (n, d), 1.0, dtype)
+    W = _normal(rng, (vocab, d), 1.0 / math.sqrt(d), dtype)
+    return h, W

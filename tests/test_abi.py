@@ -28,7 +28,8 @@ def test_header_declares_the_entry_points():
     assert _declared() == sorted([
         "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
         "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
-        "fovea_last_error", "fovea_profile", "fovea_profile_read"])
+        "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
+        "fovea_lm_topk"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -95,4 +96,17 @@ def test_null_context_paths(lib):
     assert lib.lib.fovea_last_error(None, None, None) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_profile(None, 1) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_profile_read(None, 4, None, None, None) == -1
+    assert lib.lib.fovea_lm_topk_workspace(None, 4, 32000, 6) == 0
+    assert lib.lib.fovea_lm_topk(None, 4, None, None, 32000, 6, None, None, None, 0,
+                                 None) == lib.FOVEA_ERR_INVALID_ARG
     lib.lib.fovea_destroy(None)
+
+
+def test_header_limits_match_the_binding(lib):
+    src = open(HEADER).read()
+    for name in ("FOVEA_MAX_M", "FOVEA_MAX_KMAX", "FOVEA_LM_MAX_K", "FOVEA_LM_MAX_VOCAB",
+                 "FOVEA_LM_MAX_ROWS"):
+        m = re.search(r"#define\s+" + name + r"\s+\(?([0-9]+)(?:\s*<<\s*([0-9]+))?", src)
+        assert m, name
+        val = int(m.group(1)) << int(m.group(2) or 0)
+        assert getattr(lib, name) == val, name

@@ -448,3 +448,81 @@ def test_stress_flat_and_peaked_halves():
     K = out["K"].reshape(wl.B, -1)
     assert (K[:4] == wl.k_max).all()
     assert (K[4:] <= 4).all()
+
+
+# ---------------------------------------------------------------------------------
+# LM head + draft candidates (Eq. hidden_correction's z_n, Algorithm 1's expansion)
+# ---------------------------------------------------------------------------------
+
+
+def _brute_lm_topk(h, W, k):
+    """Pure-Python dot products and k arg-max scans (first index wins a tie)."""
+    out = []
+    for row in h.tolist():
+        z = [sum(a * b for a, b in zip(row, w)) for w in W.tolist()]
+        taken, pick = set(), []
+        for _ in range(k):
+            best = None
+            for j, v in enumerate(z):
+                if j in taken or v != v:
+                    continue
+                if best is None or v > z[best]:
+                    best = j
+            if best is None:
+                pick.append((-1, -math.inf))
+                continue
+            taken.add(best)
+            pick.append((best, z[best]))
+        out.append(pick)
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_lm_topk_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n, d, vocab, k = 5, 12, 40, 6
+    h = rng.standard_normal((n, d))
+    W = rng.standard_normal((vocab, d))
+    idx, val = oracle.lm_topk(h, W, k)
+    ref = _brute_lm_topk(h, W, k)
+    for r in range(n):
+        assert idx[r].tolist() == [p[0] for p in ref[r]]
+        np.testing.assert_allclose(val[r], [p[1] for p in ref[r]], rtol=1e-12, atol=1e-12)
+
+
+def test_lm_topk_exact_ties_break_to_lower_id():
+    # duplicated head rows give bit-identical logits: the lower token id ranks first
+    rng = np.random.default_rng(3)
+    d, vocab = 8, 30
+    W = rng.standard_normal((vocab, d))
+    W[17] = W[4]
+    W[25] = W[4]
+    W[9] = W[2]
+    h = np.stack([W[4] * 3.0, W[2] * 3.0])  # rows 4 / 2 (and their copies) score highest
+    idx, val = oracle.lm_topk(h, W, 4)
+    assert idx[0, :3].tolist() == [4, 17, 25]
+    assert val[0, 0] == val[0, 1] == val[0, 2]
+    assert idx[1, :2].tolist() == [2, 9]
+    ref = _brute_lm_topk(h, W, 4)
+    assert idx.tolist() == [[p[0] for p in r] for r in ref]
+
+
+def test_lm_topk_full_sort_and_k1_argmax():
+    rng = np.random.default_rng(4)
+    h = rng.standard_normal((3, 16))
+    W = rng.standard_normal((12, 16))
+    z = h @ W.T
+    idx, val = oracle.lm_topk(h, W, 12)
+    for r in range(3):
+        assert idx[r].tolist() == sorted(range(12), key=lambda j: (-z[r, j], j))
+        assert np.all(np.diff(val[r]) <= 0)
+    idx1, _ = oracle.lm_topk(h, W, 1)
+    assert idx1[:, 0].tolist() == np.argmax(z, axis=1).tolist()
+
+
+def test_lm_topk_nan_logits_are_skipped():
+    h = np.array([[1.0, 0.0], [np.nan, 0.0]])
+    W = np.array([[1.0, 0.0], [2.0, 0.0], [np.nan, 0.0], [0.5, 0.0]])
+    idx, val = oracle.lm_topk(h, W, 4)
+    assert idx[0].tolist() == [1, 0, 3, -1] and val[0, 3] == -np.inf
+    assert idx[1].tolist() == [-1, -1, -1, -1]
