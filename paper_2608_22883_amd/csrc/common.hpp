@@ -161,6 +161,18 @@ __device__ __forceinline__ int wave_sum_i32(int v) {
 }
 
 // Inclusive prefix sum over the 64 lanes (DPP row shifts, then row broadcasts).
+// Inclusive prefix sum within each row of 16 lanes (the row-local steps of the wave scan
+// below); every lane of the row must be active.
+__device__ __forceinline__ int row16_incl_scan_i32(int v) {
+  const int x = v;
+  v += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, x, 0x113, 0xF, 0xF, false);  // row_shr:3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xE, false);  // row_shr:4, banks 1-3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xC, false);  // row_shr:8, banks 2-3
+  return v;
+}
+
 __device__ __forceinline__ int wave_incl_scan_i32(int v) {
   const int x = v;
   v += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1

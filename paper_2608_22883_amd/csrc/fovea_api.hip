@@ -439,11 +439,11 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
 
 size_t lm_cand_bytes(int n, int vocab, int k) {
   const size_t cb = (static_cast<size_t>(vocab) + 127) / 128;
-  return align_up(static_cast<size_t>(n) * cb * k * sizeof(LmCand));
+  return align_up(static_cast<size_t>(n) * cb * k * sizeof(uint64_t));
 }
 
 template <typename T, int BM>
-void launch_lm(int n, const T* h, int d, const T* W, int vocab, int k, LmCand* cand,
+void launch_lm(int n, const T* h, int d, const T* W, int vocab, int k, uint64_t* cand,
                hipStream_t s) {
   const LmMap m = make_lm_map((n + BM - 1) / BM, (vocab + 127) / 128);
   hipLaunchKernelGGL((lm_kernel<T, BM>), dim3(lm_grid(m)), dim3(256), 0, s, m, n, h, d, W, vocab,
@@ -452,7 +452,7 @@ void launch_lm(int n, const T* h, int d, const T* W, int vocab, int k, LmCand* c
 
 template <typename T>
 fovea_status run_lm_topk(fovea_ctx* c, int n, const void* h, const void* W, int vocab, int k,
-                         int32_t* idx, float* logit, LmCand* cand, hipStream_t s) {
+                         int32_t* idx, float* logit, uint64_t* cand, hipStream_t s) {
   const int d = c->dims.d;
   {
     ProfScope ps(c, kLmHead, s);
@@ -739,7 +739,7 @@ fovea_status fovea_lm_topk(fovea_ctx* c, int32_t n_rows, const void* h, const vo
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
   if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
-  LmCand* cand = static_cast<LmCand*>(workspace);
+  uint64_t* cand = static_cast<uint64_t*>(workspace);
   return c->bf16 ? run_lm_topk<bf16_t>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream)
                  : run_lm_topk<float>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream);
 }
