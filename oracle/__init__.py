@@ -30,6 +30,7 @@ from .fovea_ref import (  # noqa: F401
     query,
     readout,
     retrieve_fuse,
+    retrieve_fuse_backward,
     rms_norm,
     scores,
     select_cumulative_mass,

@@ -16,6 +16,11 @@ Sources (paper section / equation):
     nets two biased linear layers with a 512-wide SiLU hidden layer; the scalar gate is
     broadcast over the hidden size; h_hat = RMSNorm(h_n + g_n c_n) (Eq. hidden_correction).
   * Algorithm 1 orders the per-node steps the same way.
+  * Training the module (Method, training objective; appendix, draft model training):
+    ``retrieve_fuse_backward`` takes dL/dh_hat and returns the gradients of the states,
+    the memory and every per-step weight, by the chain rule through RMSNorm, the gated
+    residual, both nets, the renormalised softmax over the selected set and the query;
+    the selected set itself is held fixed (it is a discrete choice).
   * Eq. hidden_correction's z_n = W_LM h_hat_n and Algorithm 1's tree expansion, which
     adds each node's K_c highest-scoring tokens (K_c = 6 in the experimental setup):
     ``lm_topk``.
@@ -38,7 +43,9 @@ scaled-dot-product attention, LayerNorm/RMSNorm/linear against torch.nn.function
 the peaked case (K = 1, readout equals the value row exactly), gate = 0 and gate = 1
 special cases, invariants (mass, clamps, permutation equivariance, masking); for
 ``lm_topk``, pure-Python brute force (dot products and repeated arg-max scans),
-exact ties from duplicated head rows, and the k = vocab case as a full sort.  The
+exact ties from duplicated head rows, and the k = vocab case as a full sort; for
+``retrieve_fuse_backward``, central finite differences of the forward in fp64, an
+autograd re-derivation in torch (fp64, CPU), and the gate-closed and no-RMSNorm cases.  The
 correction MLPs at random weights have no independent numeric fixture in the paper:
 they are pinned through the gate special cases and the torch cross-check of each
 linear layer, not through a printed example.
@@ -64,6 +71,7 @@ __all__ = [
     "correction",
     "fuse",
     "retrieve_fuse",
+    "retrieve_fuse_backward",
     "lm_logits",
     "lm_topk",
     "lm_topk_from_logits",
@@ -309,3 +317,131 @@ def lm_topk_from_logits(z, k):
         idx[r, : order.size] = order
         val[r, : order.size] = z[r][order]
     return idx, val
+
+
+def retrieve_fuse_backward(W, mem_off, keys, values, node_off, h, depth, idx, K, dh_hat):
+    """Gradients of one draft step's output h_hat with respect to its inputs and weights,
+    given dL/dh_hat (Method, training objective: the module is trained end to end; the
+    selected sets I_n = idx[n, :K[n]] are held fixed, a discrete choice with no
+    gradient).  fp64 throughout, no weight rounding.
+
+    Forward (per node n, request b, y = [h; r]):
+      x   = LN_q(h),  q = W_Q (x + E_dep[l]),  s_i = q . k_i / sqrt(d_m)  (i in I_n)
+      a_i = softmax over I_n of s,  r = sum_i a_i u_i
+      z_c = W_c1 y + b_c1,  c = W_c2 SiLU(z_c) + b_c2
+      z_g = W_g1 y + b_g1,  g = sigmoid(w_g2 . SiLU(z_g) + b_g2)
+      h'  = h + g c,  h_hat = h' rho w  (rho = 1/sqrt(mean(h'^2) + eps); rms_w None: h' )
+    Returns a dict with dh [n, d], dkeys and dvalues [n_mem, d_m], and dW_Q, dq_ln_g,
+    dq_ln_b, dE_dep, dW_c1, db_c1, dW_c2, db_c2, dW_g1, db_g1, dw_g2, db_g2, drms_w
+    (None without RMSNorm), each shaped like its weight."""
+    f = np.float64
+    h = np.asarray(h, f)
+    n, d = h.shape
+    keys = np.asarray(keys, f)
+    values = np.asarray(values, f)
+    d_m = keys.shape[1]
+    dh_hat = np.asarray(dh_hat, f)
+    depth = np.asarray(depth, np.int64)
+    W_Q, E_dep = np.asarray(W["W_Q"], f), np.asarray(W["E_dep"], f)
+    g_q, b_q = np.asarray(W["q_ln_g"], f), np.asarray(W["q_ln_b"], f)
+    W_c1, b_c1 = np.asarray(W["W_c1"], f), np.asarray(W["b_c1"], f)
+    W_c2, b_c2 = np.asarray(W["W_c2"], f), np.asarray(W["b_c2"], f)
+    W_g1, b_g1 = np.asarray(W["W_g1"], f), np.asarray(W["b_g1"], f)
+    w_g2, b_g2 = np.asarray(W["w_g2"], f), float(W["b_g2"])
+    rms_w = W.get("rms_w")
+    eps_ln, eps_rms = W["ln_eps"], W["rms_eps"]
+    scale = 1.0 / np.sqrt(d_m)
+    # request of every node, global memory rows of every selected entry
+    req = np.zeros(n, np.int64)
+    for b in range(len(node_off) - 1):
+        req[int(node_off[b]):int(node_off[b + 1])] = b
+
+    # ---- forward, keeping what the chain rule needs
+    mu = h.mean(axis=1, keepdims=True)
+    rstd = 1.0 / np.sqrt(((h - mu) ** 2).mean(axis=1, keepdims=True) + eps_ln)
+    xhat = (h - mu) * rstd
+    xe = xhat * g_q + b_q + E_dep[depth]
+    q = xe @ W_Q.T
+    r = np.zeros((n, d_m))
+    sel, alpha = [], []
+    for i in range(n):
+        rows = int(mem_off[req[i]]) + np.asarray(idx[i][: int(K[i])], np.int64)
+        sel.append(rows)
+        if rows.size == 0:
+            alpha.append(np.zeros(0))
+            continue
+        s_i = keys[rows] @ q[i] * scale
+        e = np.exp(s_i - s_i.max())
+        a = e / e.sum()
+        alpha.append(a)
+        r[i] = a @ values[rows]
+    y = np.concatenate([h, r], axis=1)
+    z_c = y @ W_c1.T + b_c1
+    a_c = silu(z_c)
+    c = a_c @ W_c2.T + b_c2
+    z_g = y @ W_g1.T + b_g1
+    a_g = silu(z_g)
+    g = sigmoid(a_g @ w_g2 + b_g2)
+    hp = h + g[:, None] * c
+
+    def dsilu(z):  # d/dz z sigmoid(z)
+        sg = sigmoid(z)
+        return sg * (1.0 + z * (1.0 - sg))
+
+    # ---- RMSNorm: h_hat = h' rho w
+    if rms_w is None:
+        dhp = dh_hat
+        drms = None
+    else:
+        w = np.asarray(rms_w, f)
+        rho = 1.0 / np.sqrt((hp * hp).mean(axis=1, keepdims=True) + eps_rms)
+        drms = (dh_hat * hp * rho).sum(axis=0)
+        gw = dh_hat * w
+        dhp = rho * gw - rho ** 3 * hp * (gw * hp).sum(axis=1, keepdims=True) / d
+    # ---- gated residual h' = h + g c
+    dh = dhp.copy()
+    dc = g[:, None] * dhp
+    dg = (dhp * c).sum(axis=1)
+    dlogit = dg * g * (1.0 - g)
+    # ---- layer 2 and the gate's second layer
+    dW_c2 = dc.T @ a_c
+    db_c2 = dc.sum(axis=0)
+    dz_c = (dc @ W_c2) * dsilu(z_c)
+    dw_g2 = a_g.T @ dlogit
+    db_g2 = dlogit.sum()
+    dz_g = dlogit[:, None] * w_g2[None, :] * dsilu(z_g)
+    # ---- first layers over y = [h; r]
+    dW_c1 = dz_c.T @ y
+    db_c1 = dz_c.sum(axis=0)
+    dW_g1 = dz_g.T @ y
+    db_g1 = dz_g.sum(axis=0)
+    dy = dz_c @ W_c1 + dz_g @ W_g1
+    dh += dy[:, :d]
+    dr = dy[:, d:]
+    # ---- readout r = sum a_i u_i, a = softmax over the selected set of s
+    dkeys = np.zeros_like(keys)
+    dvalues = np.zeros_like(values)
+    dq = np.zeros((n, d_m))
+    for i in range(n):
+        rows, a = sel[i], alpha[i]
+        if rows.size == 0:
+            continue
+        da = values[rows] @ dr[i]
+        ds = a * (da - a @ da)
+        np.add.at(dvalues, rows, a[:, None] * dr[i][None, :])
+        dq[i] = ds @ keys[rows] * scale
+        np.add.at(dkeys, rows, ds[:, None] * q[i][None, :] * scale)
+    # ---- query q = W_Q (LN(h) g + b + E_dep[l])
+    dW_Q = dq.T @ xe
+    dxe = dq @ W_Q
+    dE_dep = np.zeros_like(E_dep)
+    np.add.at(dE_dep, depth, dxe)
+    dq_ln_g = (dxe * xhat).sum(axis=0)
+    dq_ln_b = dxe.sum(axis=0)
+    dxh = dxe * g_q
+    dh += rstd * (dxh - dxh.mean(axis=1, keepdims=True)
+                  - xhat * (dxh * xhat).mean(axis=1, keepdims=True))
+    return dict(dh=dh, dkeys=dkeys, dvalues=dvalues, dW_Q=dW_Q, dq_ln_g=dq_ln_g,
+                dq_ln_b=dq_ln_b, dE_dep=dE_dep, dW_c1=dW_c1, db_c1=db_c1, dW_c2=dW_c2,
+                db_c2=db_c2, dW_g1=dW_g1, db_g1=db_g1, dw_g2=dw_g2, db_g2=db_g2,
+                drms_w=drms)
