@@ -160,6 +160,62 @@ fovea_status fovea_retrieve_fuse(fovea_ctx* ctx, int32_t B, const int64_t* mem_o
                                  float* r_out, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* Sticky bit of fovea_retrieve_fuse_backward: a node's K or selected index is outside
+ * [0, min(k_max, M_b)] / [0, M_b) (its gradients are skipped and its dh row is NaN). */
+#define FOVEA_DATA_BAD_SELECTION 0x10u
+
+/* Gradient outputs of fovea_retrieve_fuse_backward: fp32 device arrays shaped like the
+ * weights of fovea_params (raw, unfolded), overwritten.  rms_w is required exactly when
+ * the weights passed have an RMSNorm weight. */
+typedef struct {
+  float* W_Q;    /* [d_m, d] */
+  float* q_ln_g; /* [d] */
+  float* q_ln_b; /* [d] */
+  float* E_dep;  /* [n_depth, d] */
+  float* W_c1;   /* [d_c, d + d_m] */
+  float* b_c1;   /* [d_c] */
+  float* W_c2;   /* [d, d_c] */
+  float* b_c2;   /* [d] */
+  float* W_g1;   /* [d_c, d + d_m] */
+  float* b_g1;   /* [d_c] */
+  float* w_g2;   /* [d_c] */
+  float* b_g2;   /* [1] */
+  float* rms_w;  /* [d] or NULL */
+} fovea_grads;
+
+/* Bytes of workspace fovea_retrieve_fuse_backward needs (0 on bad arguments). */
+size_t fovea_retrieve_fuse_backward_workspace(const fovea_ctx* ctx, int32_t B,
+                                              int32_t n_nodes_total, int32_t k_max);
+
+/* Backward of one draft step, for training the module (Method, training objective;
+ * appendix, draft model training, where the retrieval cardinality is held at K_r = 16):
+ * given dL/dh_hat, the gradients of the states, the memory and every per-step weight.
+ * The selected sets are a discrete choice and are held fixed: the caller passes the
+ * forward's K and idx (fovea_retrieve_fuse's k_out and idx_out, local indices).
+ * Requires a context created with dtype FOVEA_F32; all arithmetic is fp32.
+ *   params   the raw (unfolded) weights as fp32 device arrays, as given to fovea_create
+ *            (the memory-build weights are not read); b_g2 and rms_w as there.
+ *   B, mem_off, n_mem_total, m_max, keys, values, node_off, n_nodes_total, t_max, h,
+ *   depth    as for fovea_retrieve_fuse (fp32 arrays).
+ *   K        [n_nodes_total] int32, idx [n_nodes_total, k_max] int32: the selection.
+ *   dh_hat   [n_nodes_total, d] fp32: dL/dh_hat.
+ * Outputs (fp32 device arrays, overwritten):
+ *   dh       [n_nodes_total, d]   dL/dh (through the retrieval and the correction).
+ *   dkeys, dvalues [n_mem_total, d_m]: dL/dk_i, dL/du_i (zero for unselected rows;
+ *            accumulated with atomic adds, so their last bits may vary between runs).
+ *   grads    the weight gradients (see fovea_grads).
+ * Nodes that fail validation (offsets, depth, selection) contribute nothing, get a NaN
+ * dh row and set sticky bits read by fovea_last_error.  workspace: at least
+ * fovea_retrieve_fuse_backward_workspace(...) bytes, 256-byte aligned; every array
+ * 16-byte aligned. */
+fovea_status fovea_retrieve_fuse_backward(
+    fovea_ctx* ctx, const fovea_params* params, int32_t B, const int64_t* mem_off,
+    int64_t n_mem_total, int32_t m_max, const float* keys, const float* values,
+    const int32_t* node_off, int32_t n_nodes_total, int32_t t_max, const float* h,
+    const int32_t* depth, const int32_t* K, const int32_t* idx, int32_t k_max,
+    const float* dh_hat, float* dh, float* dkeys, float* dvalues, const fovea_grads* grads,
+    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Limits of the candidate extraction below. */
 #define FOVEA_LM_MAX_K 16             /* candidates per row */
 #define FOVEA_LM_MAX_VOCAB (1 << 24)  /* vocabulary size */

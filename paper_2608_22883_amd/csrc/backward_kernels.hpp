@@ -1,0 +1,449 @@
+// Backward of one draft step (paper, Method, training objective; appendix, draft model
+// training: the module is trained end to end, the selected sets are a discrete choice
+// and are held fixed).  Given dL/dh_hat it produces dL/dh, dL/dkeys, dL/dvalues and the
+// gradients of every per-step weight, in fp32, from the raw (unfolded) fp32 weights.
+//
+// Forward quantities are recomputed rather than saved by the forward (the forward
+// keeps none of them):  xhat = (h - mu) rstd, xe = xhat g_q + b_q + E_dep[l],
+// q = xe W_Q^T, alpha = softmax over I_n of q . k_i / sqrt(d_m), r = sum alpha_i u_i,
+// y = [h; r], z = y [W_c1; W_g1]^T + [b_c1; b_g1], a = SiLU(z), c = a_c W_c2^T + b_c2,
+// g = sigmoid(a_g . w_g2 + b_g2), h' = h + g c.  Then, in order:
+//   RMSNorm and gate (per node)      dh' , dc = g dh', dlogit = (dh' . c) g (1 - g),
+//                                    dz_g = dlogit w_g2 SiLU'(z_g)
+//   layer 2 (GEMM)                   dz_c = (dc W_c2) SiLU'(z_c)
+//   layer 1 (GEMM)                   [dh | dr] += dz [W_c1; W_g1]
+//   readout and scores (per node)    da_i = dr . u_i, ds_i = alpha_i (da_i - alpha . da),
+//                                    dq = sum ds_i k_i / sqrt(d_m),
+//                                    du_i += alpha_i dr, dk_i += ds_i q / sqrt(d_m)
+//   query (GEMM) and LayerNorm       dxe = dq W_Q, dh += LN backward of dxe g_q
+//   weight gradients (GEMMs over the node axis of transposed activations) and
+//   bias / gain / E_dep gradients (column sums, deterministic two-stage).
+// The scatter into dkeys / dvalues uses fp32 atomic adds (their order, and so the last
+// bits of those two outputs, can vary between runs); everything else is deterministic.
+#pragma once
+
+#include "common.hpp"
+#include "correct_kernels.hpp"
+#include "gemm.hpp"
+#include "retrieve_kernels.hpp"
+
+namespace fovea {
+
+constexpr uint32_t kErrSelection = 0x10u;  // K or an index outside the request's memory
+constexpr int kColChunks = 64;             // row chunks of the column sums
+constexpr int kColGroups = 8;              // groups (depths) per column-sum pass
+
+__device__ __forceinline__ float dsilu_f(float z) {
+  const float s = sigmoid_f(z);
+  return s * (1.0f + z * (1.0f - s));
+}
+
+// sum over the 256 threads of a block, in every thread (red: 4 floats of LDS)
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+  v = wave_sum_f32(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ __launch_bounds__(256) void fill_f32_kernel(int64_t count, float* __restrict__ p, float v) {
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < count; i += static_cast<int64_t>(gridDim.x) * 256)
+    p[i] = v;
+}
+
+// dst[c * ldd + r] = src[r * lds + c] for r < R, and 0 for R <= r < R_pad (c < C);
+// 64 x 64 tiles through LDS.  Grid: (ceil(C / 64), ceil(R_pad / 64)).
+__global__ __launch_bounds__(256) void transpose_f32_kernel(int R, int R_pad, int C,
+                                                            const float* __restrict__ src,
+                                                            int64_t lds, float* __restrict__ dst,
+                                                            int64_t ldd) {
+  __shared__ float t[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    t[i][tx] = (r < R && c < C) ? src[static_cast<int64_t>(r) * lds + c] : 0.f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < C && r < R_pad) dst[static_cast<int64_t>(c) * ldd + r] = t[tx][i];
+  }
+}
+
+// Per node: xhat and xe = xhat g_q + b_q + E_dep[l], and h into y[:, :d] (ld d + d_m).
+// Rows of nodes that failed validation are written as zeros.
+__global__ __launch_bounds__(256) void bwd_prep_kernel(int n, int d, int d_m,
+                                                       const float* __restrict__ h,
+                                                       const float2* __restrict__ stats,
+                                                       const int32_t* __restrict__ node_req,
+                                                       const int32_t* __restrict__ depth, int n_depth,
+                                                       const float* __restrict__ g_q,
+                                                       const float* __restrict__ b_q,
+                                                       const float* __restrict__ E_dep,
+                                                       float* __restrict__ xhat,
+                                                       float* __restrict__ xe,
+                                                       float* __restrict__ y) {
+  const int row = blockIdx.x;
+  const bool ok = node_req[row] >= 0;
+  const float2 st = stats[row];
+  const int l = min(max(depth[row], 0), n_depth - 1);
+  const float* hr = h + static_cast<int64_t>(row) * d;
+  const float* er = E_dep + static_cast<int64_t>(l) * d;
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float x = ok ? (hr[j] - st.x) * st.y : 0.f;
+    xhat[static_cast<int64_t>(row) * d + j] = x;
+    xe[static_cast<int64_t>(row) * d + j] = ok ? fmaf(x, g_q[j], b_q[j] + er[j]) : 0.f;
+    y[static_cast<int64_t>(row) * (d + d_m) + j] = ok ? hr[j] : 0.f;
+  }
+}
+
+// Per node (one block): validates its K and indices, then recomputes the renormalised
+// softmax over the selected entries (alpha [n, k_max]) and the readout r into
+// y[:, d:].  ok[n] = 0 marks a node that failed validation (here or in the statistics
+// kernel); it contributes nothing to any gradient and its dh row becomes NaN.
+__global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m, int k_max,
+                                                          const NodeInfo* __restrict__ info,
+                                                          const int32_t* __restrict__ K_in,
+                                                          const int32_t* __restrict__ idx,
+                                                          const float* __restrict__ q,
+                                                          const float* __restrict__ keys,
+                                                          const float* __restrict__ values,
+                                                          float scale, float* __restrict__ alpha,
+                                                          float* __restrict__ y,
+                                                          int32_t* __restrict__ ok_out,
+                                                          uint32_t* err) {
+  extern __shared__ float smem_f[];
+  float* sq = smem_f;             // q_n [d_m]
+  float* sa = smem_f + d_m;       // scores, then alpha [k_max]
+  __shared__ float red[4];
+  __shared__ int sbad;
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const NodeInfo ni = info[row];
+  int K = K_in[row];
+  if (tid == 0) sbad = 0;
+  __syncthreads();
+  bool ok = ni.M >= 0;
+  if (ok && (K < 0 || K > min(k_max, ni.M))) {
+    ok = false;
+    if (tid == 0) atomicOr(err, kErrSelection);
+  }
+  if (ok) {
+    for (int i = tid; i < K; i += 256) {
+      const int ix = idx[static_cast<int64_t>(row) * k_max + i];
+      if (ix < 0 || ix >= ni.M) sbad = 1;
+    }
+  }
+  __syncthreads();
+  if (ok && sbad) {
+    ok = false;
+    if (tid == 0) atomicOr(err, kErrSelection);
+  }
+  if (tid == 0) ok_out[row] = ok ? 1 : 0;
+  if (!ok) K = 0;
+  for (int j = tid; j < d_m; j += 256) sq[j] = q[static_cast<int64_t>(row) * d_m + j];
+  __syncthreads();
+  // scores of the selected entries, one wave per entry
+  for (int i = wave; i < K; i += 4) {
+    const int64_t kr = ni.m0 + idx[static_cast<int64_t>(row) * k_max + i];
+    const float* kp = keys + kr * d_m;
+    float s = 0.f;
+    for (int j = lane; j < d_m; j += 64) s = fmaf(sq[j], kp[j], s);
+    s = wave_sum_f32(s);
+    if (lane == 0) sa[i] = s * scale;
+  }
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int i = tid; i < K; i += 256) mx = fmaxf(mx, sa[i]);
+  mx = wave_max(mx);
+  __syncthreads();
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float z = 0.f;
+  for (int i = tid; i < K; i += 256) z += expf(sa[i] - mx);
+  z = block_sum256(z, red);
+  for (int i = tid; i < K; i += 256) {
+    const float a = expf(sa[i] - mx) / z;
+    sa[i] = a;
+    alpha[static_cast<int64_t>(row) * k_max + i] = a;
+  }
+  __syncthreads();
+  // r = sum alpha_i u_i, columns over the threads
+  for (int j = tid; j < d_m; j += 256) {
+    float r = 0.f;
+    for (int i = 0; i < K; ++i)
+      r = fmaf(sa[i], values[(ni.m0 + idx[static_cast<int64_t>(row) * k_max + i]) * d_m + j], r);
+    y[static_cast<int64_t>(row) * (d + d_m) + d + j] = r;
+  }
+}
+
+// Per node: gate, h' = h + g c, RMSNorm backward, the residual split and the gate's
+// backward.  Writes dh (= dh'), dc = g dh', hn = h' rho (for dL/drms_w), dlogit[row] and
+// dz[:, d_c:] = dlogit w_g2 SiLU'(z_g).  Nodes with ok = 0 get zero gradients.
+__global__ __launch_bounds__(256) void bwd_rms_gate_kernel(int n, int d, int d_c,
+                                                           const float* __restrict__ h,
+                                                           const float* __restrict__ c,
+                                                           const float* __restrict__ z,
+                                                           const float* __restrict__ a,
+                                                           const float* __restrict__ w_g2, float b_g2,
+                                                           const float* __restrict__ rms_w, float eps,
+                                                           const float* __restrict__ dh_hat,
+                                                           const int32_t* __restrict__ ok_in,
+                                                           float* __restrict__ dh,
+                                                           float* __restrict__ dc,
+                                                           float* __restrict__ hn,
+                                                           float* __restrict__ dlogit,
+                                                           float* __restrict__ dz) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const bool ok = ok_in[row] != 0;
+  const int64_t ro = static_cast<int64_t>(row) * d;
+  const int64_t zo = static_cast<int64_t>(row) * 2 * d_c;
+  float t = 0.f;
+  for (int j = tid; j < d_c; j += 256) t = fmaf(a[zo + d_c + j], w_g2[j], t);
+  const float g = sigmoid_f(block_sum256(t, red) + b_g2);
+  float rho = 1.f, tw = 0.f;
+  if (rms_w != nullptr) {
+    float ss = 0.f, sw = 0.f;
+    for (int j = tid; j < d; j += 256) {
+      const float hp = fmaf(g, c[ro + j], h[ro + j]);
+      ss = fmaf(hp, hp, ss);
+      sw = fmaf(rms_w[j] * dh_hat[ro + j], hp, sw);
+    }
+    ss = block_sum256(ss, red);
+    tw = block_sum256(sw, red);
+    rho = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+  }
+  const float k3 = rho * rho * rho * tw / static_cast<float>(d);
+  float sdg = 0.f;
+  for (int j = tid; j < d; j += 256) {
+    const float hp = fmaf(g, c[ro + j], h[ro + j]);
+    float dhp;
+    if (rms_w != nullptr) {
+      dhp = rho * rms_w[j] * dh_hat[ro + j] - k3 * hp;
+      hn[ro + j] = ok ? hp * rho : 0.f;
+    } else {
+      dhp = dh_hat[ro + j];
+    }
+    dhp = ok ? dhp : 0.f;
+    dh[ro + j] = dhp;
+    dc[ro + j] = g * dhp;
+    sdg = fmaf(dhp, c[ro + j], sdg);
+  }
+  const float dl = block_sum256(sdg, red) * g * (1.0f - g);
+  if (tid == 0) dlogit[row] = dl;
+  for (int j = tid; j < d_c; j += 256) dz[zo + d_c + j] = dl * w_g2[j] * dsilu_f(z[zo + d_c + j]);
+}
+
+// Per node: the readout and score backward.  dr [n, d_m]; writes dq [n, d_m] and adds
+// alpha_i dr into dvalues and ds_i q / sqrt(d_m) into dkeys (atomic, fp32).
+__global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
+                                                      const NodeInfo* __restrict__ info,
+                                                      const int32_t* __restrict__ K_in,
+                                                      const int32_t* __restrict__ idx,
+                                                      const int32_t* __restrict__ ok_in,
+                                                      const float* __restrict__ alpha,
+                                                      const float* __restrict__ q,
+                                                      const float* __restrict__ dr,
+                                                      const float* __restrict__ keys,
+                                                      const float* __restrict__ values,
+                                                      float scale, float* __restrict__ dq,
+                                                      float* __restrict__ dkeys,
+                                                      float* __restrict__ dvalues) {
+  extern __shared__ float smem_f[];
+  float* sdr = smem_f;            // dr_n [d_m]
+  float* sq = smem_f + d_m;       // q_n [d_m]
+  float* sds = smem_f + 2 * d_m;  // da, then ds [k_max]
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = ok_in[row] ? K_in[row] : 0;
+  const int64_t m0 = info[row].m0;
+  const int32_t* ix = idx + static_cast<int64_t>(row) * k_max;
+  const float* al = alpha + static_cast<int64_t>(row) * k_max;
+  for (int j = tid; j < d_m; j += 256) {
+    sdr[j] = dr[static_cast<int64_t>(row) * d_m + j];
+    sq[j] = q[static_cast<int64_t>(row) * d_m + j];
+  }
+  __syncthreads();
+  for (int i = wave; i < K; i += 4) {
+    const float* up = values + (m0 + ix[i]) * d_m;
+    float s = 0.f;
+    for (int j = lane; j < d_m; j += 64) s = fmaf(sdr[j], up[j], s);
+    s = wave_sum_f32(s);
+    if (lane == 0) sds[i] = s;
+  }
+  __syncthreads();
+  float ad = 0.f;
+  for (int i = tid; i < K; i += 256) ad = fmaf(al[i], sds[i], ad);
+  ad = block_sum256(ad, red);
+  for (int i = tid; i < K; i += 256) sds[i] = al[i] * (sds[i] - ad);
+  __syncthreads();
+  for (int j = tid; j < d_m; j += 256) {
+    float acc = 0.f;
+    const float drj = sdr[j], qj = sq[j] * scale;
+    for (int i = 0; i < K; ++i) {
+      const int64_t mr = (m0 + ix[i]) * d_m + j;
+      acc = fmaf(sds[i], keys[mr], acc);
+      atomicAdd(dvalues + mr, al[i] * drj);
+      atomicAdd(dkeys + mr, sds[i] * qj);
+    }
+    dq[static_cast<int64_t>(row) * d_m + j] = acc * scale;
+  }
+}
+
+// Per node: dh += LayerNorm backward of dxe g_q (xhat, rstd); rows of nodes with
+// ok = 0 become NaN.
+__global__ __launch_bounds__(256) void bwd_ln_kernel(int n, int d, const float* __restrict__ dxe,
+                                                     const float* __restrict__ xhat,
+                                                     const float* __restrict__ g_q,
+                                                     const float2* __restrict__ stats,
+                                                     const int32_t* __restrict__ ok_in,
+                                                     float* __restrict__ dh) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int64_t ro = static_cast<int64_t>(row) * d;
+  float s1 = 0.f, s2 = 0.f;
+  for (int j = tid; j < d; j += 256) {
+    const float t = dxe[ro + j] * g_q[j];
+    s1 += t;
+    s2 = fmaf(t, xhat[ro + j], s2);
+  }
+  const float m1 = block_sum256(s1, red) / static_cast<float>(d);
+  const float m2 = block_sum256(s2, red) / static_cast<float>(d);
+  const float rstd = stats[row].y;
+  const bool ok = ok_in[row] != 0;
+  for (int j = tid; j < d; j += 256) {
+    const float t = dxe[ro + j] * g_q[j];
+    dh[ro + j] = ok ? dh[ro + j] + rstd * (t - m1 - xhat[ro + j] * m2) : __builtin_nanf("");
+  }
+}
+
+// out[j] = sum_i X[j * ldx + i] (* s[i]) over i < len: one wave per row of a transposed
+// (node-minor, zero-padded) array.
+__global__ __launch_bounds__(256) void rowsum_kernel(int rows, int len, const float* __restrict__ X,
+                                                     int64_t ldx, const float* __restrict__ s,
+                                                     float* __restrict__ out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float* xr = X + static_cast<int64_t>(r) * ldx;
+  float acc = 0.f;
+  for (int i = lane; i < len; i += 64) acc = fmaf(xr[i], s ? s[i] : 1.f, acc);
+  acc = wave_sum_f32(acc);
+  if (lane == 0) out[r] = acc;
+}
+
+// Column sums, stage 1: part[chunk][g][j] = sum over the chunk's rows i with
+// grp[i] - g0 == g of X[i][j] (* Y[i][j]); grid (ceil(cols / 256), kColChunks).
+__global__ __launch_bounds__(256) void colsum_part_kernel(int n, int cols, const float* __restrict__ X,
+                                                          int64_t ldx, const float* __restrict__ Y,
+                                                          int64_t ldy, const int32_t* __restrict__ grp,
+                                                          int g0, int ng, int n_grp_total,
+                                                          float* __restrict__ part) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  const int per = (n + kColChunks - 1) / kColChunks;
+  const int i0 = blockIdx.y * per, i1 = min(n, i0 + per);
+  float acc[kColGroups];
+#pragma unroll
+  for (int g = 0; g < kColGroups; ++g) acc[g] = 0.f;
+  if (j < cols) {
+    for (int i = i0; i < i1; ++i) {
+      float v = X[static_cast<int64_t>(i) * ldx + j];
+      if (Y != nullptr) v *= Y[static_cast<int64_t>(i) * ldy + j];
+      const int g = grp ? min(max(grp[i], 0), n_grp_total - 1) - g0 : 0;
+#pragma unroll
+      for (int gg = 0; gg < kColGroups; ++gg) acc[gg] += gg == g ? v : 0.f;
+    }
+#pragma unroll
+    for (int g = 0; g < kColGroups; ++g)
+      if (g < ng) part[(static_cast<int64_t>(blockIdx.y) * kColGroups + g) * cols + j] = acc[g];
+  }
+}
+
+// Column sums, stage 2: out[(g0 + g) * cols + j] = sum over chunks (fixed order).
+__global__ __launch_bounds__(256) void colsum_final_kernel(int cols, int g0, int ng,
+                                                           const float* __restrict__ part,
+                                                           float* __restrict__ out) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  const int g = blockIdx.y;
+  if (j >= cols || g >= ng) return;
+  float acc = 0.f;
+  for (int ch = 0; ch < kColChunks; ++ch)
+    acc += part[(static_cast<int64_t>(ch) * kColGroups + g) * cols + j];
+  out[static_cast<int64_t>(g0 + g) * cols + j] = acc;
+}
+
+// fp32 GEMM C = A B^T (A [M, K], B [N, K], K a multiple of 32, N a multiple of 8) on the
+// gemm.hpp core, with the epilogues the backward needs.
+enum BwdEpi : int {
+  kEpiStore = 0,  // out = v (+ bias[col])
+  kEpiZ = 1,      // out = v + bias (pre-activation), out2 = SiLU(out)
+  kEpiDsilu = 2,  // out = v * SiLU'(aux)
+  kEpiSplit = 3,  // col < split: out[col] += v; else out2[col - split] = v
+};
+
+struct BwdGemm {
+  int M, N, K;
+  const float* A;
+  int64_t lda;
+  const float* B;
+  int64_t ldb;
+  float* out;
+  int64_t ldo;
+  const float* bias;
+  float* out2;
+  int64_t ldo2;
+  const float* aux;
+  int64_t ldaux;
+  int split;
+};
+
+template <int EPI>
+__global__ __launch_bounds__(256) void bwd_gemm_kernel(TileMap tm, BwdGemm g) {
+  using C = GemmCfg<float, 64, 2>;
+  __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
+  int tr, tc;
+  if (!tm.map(tr, tc)) return;
+  const int m0 = tr * C::BM, n0 = tc * C::BN;
+  f32x4 acc[C::TM][C::TN];
+  gemm_mainloop<C>(acc, g.A, g.lda, g.M, g.B, g.ldb, g.N, g.K, m0, n0, smem);
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8]) -> float {
+        if (row >= g.M || col0 >= g.N) return 0.f;
+        float o[8];
+        if (EPI == kEpiStore || EPI == kEpiZ) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = v[e] + (g.bias ? g.bias[col0 + e] : 0.f);
+          store8(g.out + static_cast<int64_t>(row) * g.ldo + col0, o);
+          if (EPI == kEpiZ) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = silu_f(o[e]);
+            store8(g.out2 + static_cast<int64_t>(row) * g.ldo2 + col0, o);
+          }
+        } else if (EPI == kEpiDsilu) {
+          float zz[8];
+          load8(g.aux + static_cast<int64_t>(row) * g.ldaux + col0, zz);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = v[e] * dsilu_f(zz[e]);
+          store8(g.out + static_cast<int64_t>(row) * g.ldo + col0, o);
+        } else {
+          if (col0 < g.split) {
+            float* p = g.out + static_cast<int64_t>(row) * g.ldo + col0;
+            load8(p, o);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] += v[e];
+            store8(p, o);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = v[e];
+            store8(g.out2 + static_cast<int64_t>(row) * g.ldo2 + (col0 - g.split), o);
+          }
+        }
+        return 0.f;
+      },
+      NoRowSum{});
+}
+
+}  // namespace fovea

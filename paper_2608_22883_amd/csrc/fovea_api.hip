@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "fovea.h"
+#include "backward_kernels.hpp"
 #include "correct_kernels.hpp"
 #include "lm_kernels.hpp"
 #include "retrieve_kernels.hpp"
@@ -16,6 +17,10 @@
 using namespace fovea;
 
 static_assert(FOVEA_MAX_M == kMaxM && FOVEA_MAX_KMAX == kMaxKmax, "header limits");
+static_assert(FOVEA_DATA_BAD_NODE_OFFSETS == kErrNodeOff && FOVEA_DATA_BAD_MEM_OFFSETS == kErrMemOff &&
+                  FOVEA_DATA_BAD_DEPTH == kErrDepth && FOVEA_DATA_BAD_TAU == kErrTau &&
+                  FOVEA_DATA_BAD_SELECTION == kErrSelection,
+              "error bits");
 static_assert(FOVEA_LM_MAX_K == kLmMaxK && FOVEA_LM_MAX_VOCAB == kLmMaxVocab &&
                   FOVEA_LM_MAX_ROWS == kLmMaxRows,
               "header limits");
@@ -111,11 +116,15 @@ bool dims_supported(const fovea_dims* d) {
 
 enum KernelSlot {
   kRowStats, kHq, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kLmHead, kLmMerge,
-  kNumSlots
+  kBwdFill, kBwdStats, kBwdTranspose, kBwdPrep, kBwdGemm, kBwdSelFwd, kBwdRmsGate, kBwdSel,
+  kBwdLn, kBwdReduce, kNumSlots
 };
-const char* const kSlotNames[kNumSlots] = {"row_stats", "hq",       "score",         "select_gather",
-                                           "corr1",     "corr2",    "rms",           "mem_row_stats",
-                                           "mem_proj",  "lm_head",  "lm_merge"};
+const char* const kSlotNames[kNumSlots] = {
+    "row_stats",     "hq",           "score",       "select_gather", "corr1",
+    "corr2",         "rms",          "mem_row_stats", "mem_proj",    "lm_head",
+    "lm_merge",      "bwd_fill",     "bwd_stats",   "bwd_transpose", "bwd_prep",
+    "bwd_gemm",      "bwd_sel_fwd",  "bwd_rms_gate", "bwd_sel",      "bwd_ln",
+    "bwd_reduce"};
 
 hipEvent_t prof_event(fovea_ctx* c) {
   if (!c->prof_pool.empty()) {
@@ -473,6 +482,280 @@ fovea_status run_lm_topk(fovea_ctx* c, int n, const void* h, const void* W, int 
   return hipGetLastError() == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
 }
 
+// ---------------------------------------------------------------------------------
+// backward
+// ---------------------------------------------------------------------------------
+
+struct BwdLayout {
+  int npad;
+  size_t node_req, info, stats, tau0, ok, dlogit;
+  size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe;
+  size_t xeT, yT, aT, dcT, dzT, dqT, WQT, Wc2T, W1T, part;
+  size_t total;
+};
+
+BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max) {
+  BwdLayout L;
+  const size_t d = D.d, dm = D.d_m, dc = D.d_c, nn = n;
+  const size_t np = (nn + 63) / 64 * 64;
+  L.npad = static_cast<int>(np);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  L.node_req = take(nn * 4);
+  L.info = take(nn * sizeof(NodeInfo));
+  L.stats = take(nn * 8);
+  L.tau0 = take(static_cast<size_t>(B) * 4);
+  L.ok = take(nn * 4);
+  L.dlogit = take(np * 4);
+  L.xhat = take(nn * d * 4);
+  L.xe = take(nn * d * 4);
+  L.y = take(nn * (d + dm) * 4);
+  L.q = take(nn * dm * 4);
+  L.alpha = take(nn * static_cast<size_t>(k_max) * 4);
+  L.z = take(nn * 2 * dc * 4);
+  L.a = take(nn * 2 * dc * 4);
+  L.c = take(nn * d * 4);
+  L.hn = take(nn * d * 4);
+  L.dc = take(nn * d * 4);
+  L.dz = take(nn * 2 * dc * 4);
+  L.dr = take(nn * dm * 4);
+  L.dq = take(nn * dm * 4);
+  L.dxe = take(nn * d * 4);
+  L.xeT = take(d * np * 4);
+  L.yT = take((d + dm) * np * 4);
+  L.aT = take(2 * dc * np * 4);
+  L.dcT = take(d * np * 4);
+  L.dzT = take(2 * dc * np * 4);
+  L.dqT = take(dm * np * 4);
+  L.WQT = take(d * dm * 4);
+  L.Wc2T = take(dc * d * 4);
+  L.W1T = take((d + dm) * 2 * dc * 4);
+  L.part = take(static_cast<size_t>(kColChunks) * kColGroups * std::max(d, 2 * dc) * 4);
+  L.total = o;
+  return L;
+}
+
+struct BwdArgs {
+  const fovea_params* P;
+  int B;
+  const int64_t* mem_off;
+  int64_t n_mem;
+  int m_max;
+  const float* keys;
+  const float* values;
+  const int32_t* node_off;
+  int n, t_max;
+  const float* h;
+  const int32_t* depth;
+  const int32_t* K;
+  const int32_t* idx;
+  int k_max;
+  const float* dh_hat;
+  float* dh;
+  float* dkeys;
+  float* dvalues;
+  const fovea_grads* G;
+  char* ws;
+};
+
+void launch_fill(float* p, int64_t count, hipStream_t s) {
+  if (count <= 0) return;
+  const int64_t blocks = std::min<int64_t>((count + 255) / 256, 4096);
+  hipLaunchKernelGGL(fill_f32_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, count, p, 0.f);
+}
+
+void launch_transpose(int R, int R_pad, int C, const float* src, int64_t lds, float* dst,
+                      int64_t ldd, hipStream_t s) {
+  hipLaunchKernelGGL(transpose_f32_kernel, dim3((C + 63) / 64, (R_pad + 63) / 64), dim3(256), 0, s,
+                     R, R_pad, C, src, lds, dst, ldd);
+}
+
+template <int EPI>
+void launch_bwd_gemm(const BwdGemm& g, hipStream_t s) {
+  using C = GemmCfg<float, 64, 2>;
+  const TileMap tm = make_tile_map((g.M + C::BM - 1) / C::BM, (g.N + C::BN - 1) / C::BN,
+                                   static_cast<double>(g.M) * g.K, static_cast<double>(g.N) * g.K);
+  hipLaunchKernelGGL(bwd_gemm_kernel<EPI>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+}
+
+BwdGemm bwd_gemm(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
+                 float* out, int64_t ldo) {
+  BwdGemm g{};
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.lda = lda;
+  g.B = B;
+  g.ldb = ldb;
+  g.out = out;
+  g.ldo = ldo;
+  return g;
+}
+
+void launch_colsum(int n, int cols, const float* X, int64_t ldx, const float* Y, int64_t ldy,
+                   const int32_t* grp, int n_groups, float* part, float* out, hipStream_t s) {
+  for (int g0 = 0; g0 < n_groups; g0 += kColGroups) {
+    const int ng = std::min(kColGroups, n_groups - g0);
+    hipLaunchKernelGGL(colsum_part_kernel, dim3((cols + 255) / 256, kColChunks), dim3(256), 0, s, n,
+                       cols, X, ldx, Y, ldy, grp, g0, ng, n_groups, part);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256, ng), dim3(256), 0, s, cols, g0,
+                       ng, part, out);
+  }
+}
+
+void launch_rowsum(int rows, int len, const float* X, int64_t ldx, const float* sc, float* out,
+                   hipStream_t s) {
+  hipLaunchKernelGGL(rowsum_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, rows, len, X, ldx, sc, out);
+}
+
+fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
+  const fovea_dims& D = c->dims;
+  const int n = a.n, d = D.d, dm = D.d_m, dc = D.d_c, nd = D.n_depth;
+  const BwdLayout L = bwd_layout(D, a.B, n, a.k_max);
+  const int np = L.npad;
+  char* w = a.ws;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(w + off); };
+  int32_t* node_req = reinterpret_cast<int32_t*>(w + L.node_req);
+  NodeInfo* info = reinterpret_cast<NodeInfo*>(w + L.info);
+  float2* stats = reinterpret_cast<float2*>(w + L.stats);
+  int32_t* ok = reinterpret_cast<int32_t*>(w + L.ok);
+  const float* W_Q = static_cast<const float*>(a.P->W_Q);
+  const float* W_c1 = static_cast<const float*>(a.P->W_c1);
+  const float* W_g1 = static_cast<const float*>(a.P->W_g1);
+  const float* W_c2 = static_cast<const float*>(a.P->W_c2);
+  const float* rms_w = static_cast<const float*>(a.P->rms_w);
+  const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(dm)));
+  const fovea_grads& G = *a.G;
+  // per-node kernels keep q, dr and the selection's scores in LDS
+  const size_t sm_fwd = static_cast<size_t>(dm + a.k_max) * 4;
+  const size_t sm_bwd = static_cast<size_t>(2 * dm + a.k_max) * 4;
+  FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_sel_fwd_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_fwd)));
+  FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_sel_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_bwd)));
+  {
+    ProfScope ps(c, kBwdFill, s);
+    launch_fill(F(L.tau0), a.B, s);
+    launch_fill(F(L.dlogit), np, s);
+    launch_fill(a.dkeys, a.n_mem * dm, s);
+    launch_fill(a.dvalues, a.n_mem * dm, s);
+  }
+  {
+    ProfScope ps(c, kBwdStats, s);
+    hipLaunchKernelGGL(row_stats_kernel<float>, dim3((n + 3) / 4), dim3(256), 0, s, n, a.h, d,
+                       D.ln_eps, stats, a.depth, nd, a.node_off, a.B, a.t_max, F(L.tau0), a.mem_off,
+                       a.n_mem, a.m_max, node_req, info, c->err);
+  }
+  {
+    ProfScope ps(c, kBwdTranspose, s);
+    launch_transpose(dm, dm, d, W_Q, d, F(L.WQT), dm, s);
+    launch_transpose(d, d, dc, W_c2, dc, F(L.Wc2T), d, s);
+    launch_transpose(dc, dc, d + dm, W_c1, d + dm, F(L.W1T), 2 * dc, s);
+    launch_transpose(dc, dc, d + dm, W_g1, d + dm, F(L.W1T) + dc, 2 * dc, s);
+  }
+  {
+    ProfScope ps(c, kBwdPrep, s);
+    hipLaunchKernelGGL(bwd_prep_kernel, dim3(n), dim3(256), 0, s, n, d, dm, a.h, stats, node_req,
+                       a.depth, nd, static_cast<const float*>(a.P->q_ln_g),
+                       static_cast<const float*>(a.P->q_ln_b), static_cast<const float*>(a.P->E_dep),
+                       F(L.xhat), F(L.xe), F(L.y));
+  }
+  {
+    ProfScope ps(c, kBwdGemm, s);
+    launch_bwd_gemm<kEpiStore>(bwd_gemm(n, dm, d, F(L.xe), d, W_Q, d, F(L.q), dm), s);
+  }
+  {
+    ProfScope ps(c, kBwdSelFwd, s);
+    hipLaunchKernelGGL(bwd_sel_fwd_kernel, dim3(n), dim3(256), sm_fwd, s, n, d, dm, a.k_max, info, a.K,
+                       a.idx, F(L.q), a.keys, a.values, scale, F(L.alpha), F(L.y), ok, c->err);
+  }
+  {
+    ProfScope ps(c, kBwdGemm, s);
+    BwdGemm g = bwd_gemm(n, dc, d + dm, F(L.y), d + dm, W_c1, d + dm, F(L.z), 2 * dc);
+    g.bias = static_cast<const float*>(a.P->b_c1);
+    g.out2 = F(L.a);
+    g.ldo2 = 2 * dc;
+    launch_bwd_gemm<kEpiZ>(g, s);
+    g.B = W_g1;
+    g.bias = static_cast<const float*>(a.P->b_g1);
+    g.out = F(L.z) + dc;
+    g.out2 = F(L.a) + dc;
+    launch_bwd_gemm<kEpiZ>(g, s);
+    BwdGemm g2 = bwd_gemm(n, d, dc, F(L.a), 2 * dc, W_c2, dc, F(L.c), d);
+    g2.bias = static_cast<const float*>(a.P->b_c2);
+    launch_bwd_gemm<kEpiStore>(g2, s);
+  }
+  {
+    ProfScope ps(c, kBwdRmsGate, s);
+    hipLaunchKernelGGL(bwd_rms_gate_kernel, dim3(n), dim3(256), 0, s, n, d, dc, a.h, F(L.c), F(L.z),
+                       F(L.a), static_cast<const float*>(a.P->w_g2), a.P->b_g2, rms_w, D.rms_eps,
+                       a.dh_hat, ok, a.dh, F(L.dc), F(L.hn), F(L.dlogit), F(L.dz));
+  }
+  {
+    ProfScope ps(c, kBwdGemm, s);
+    BwdGemm g = bwd_gemm(n, dc, d, F(L.dc), d, F(L.Wc2T), d, F(L.dz), 2 * dc);
+    g.aux = F(L.z);
+    g.ldaux = 2 * dc;
+    launch_bwd_gemm<kEpiDsilu>(g, s);
+    BwdGemm g2 = bwd_gemm(n, d + dm, 2 * dc, F(L.dz), 2 * dc, F(L.W1T), 2 * dc, a.dh, d);
+    g2.split = d;
+    g2.out2 = F(L.dr);
+    g2.ldo2 = dm;
+    launch_bwd_gemm<kEpiSplit>(g2, s);
+  }
+  {
+    ProfScope ps(c, kBwdSel, s);
+    hipLaunchKernelGGL(bwd_sel_kernel, dim3(n), dim3(256), sm_bwd, s, n, dm, a.k_max, info, a.K, a.idx,
+                       ok, F(L.alpha), F(L.q), F(L.dr), a.keys, a.values, scale, F(L.dq), a.dkeys,
+                       a.dvalues);
+  }
+  {
+    ProfScope ps(c, kBwdGemm, s);
+    launch_bwd_gemm<kEpiStore>(bwd_gemm(n, d, dm, F(L.dq), dm, F(L.WQT), dm, F(L.dxe), d), s);
+  }
+  {
+    ProfScope ps(c, kBwdLn, s);
+    hipLaunchKernelGGL(bwd_ln_kernel, dim3(n), dim3(256), 0, s, n, d, F(L.dxe), F(L.xhat),
+                       static_cast<const float*>(a.P->q_ln_g), stats, ok, a.dh);
+  }
+  {
+    ProfScope ps(c, kBwdTranspose, s);
+    launch_transpose(n, np, d, F(L.xe), d, F(L.xeT), np, s);
+    launch_transpose(n, np, d + dm, F(L.y), d + dm, F(L.yT), np, s);
+    launch_transpose(n, np, 2 * dc, F(L.a), 2 * dc, F(L.aT), np, s);
+    launch_transpose(n, np, d, F(L.dc), d, F(L.dcT), np, s);
+    launch_transpose(n, np, 2 * dc, F(L.dz), 2 * dc, F(L.dzT), np, s);
+    launch_transpose(n, np, dm, F(L.dq), dm, F(L.dqT), np, s);
+  }
+  {
+    ProfScope ps(c, kBwdGemm, s);
+    launch_bwd_gemm<kEpiStore>(bwd_gemm(d, dc, np, F(L.dcT), np, F(L.aT), np, G.W_c2, dc), s);
+    launch_bwd_gemm<kEpiStore>(bwd_gemm(dc, d + dm, np, F(L.dzT), np, F(L.yT), np, G.W_c1, d + dm), s);
+    launch_bwd_gemm<kEpiStore>(
+        bwd_gemm(dc, d + dm, np, F(L.dzT) + static_cast<int64_t>(dc) * np, np, F(L.yT), np, G.W_g1, d + dm), s);
+    launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, d, np, F(L.dqT), np, F(L.xeT), np, G.W_Q, d), s);
+  }
+  {
+    ProfScope ps(c, kBwdReduce, s);
+    launch_rowsum(d, np, F(L.dcT), np, nullptr, G.b_c2, s);
+    launch_rowsum(dc, np, F(L.dzT), np, nullptr, G.b_c1, s);
+    launch_rowsum(dc, np, F(L.dzT) + static_cast<int64_t>(dc) * np, np, nullptr, G.b_g1, s);
+    launch_rowsum(dc, np, F(L.aT) + static_cast<int64_t>(dc) * np, np, F(L.dlogit), G.w_g2, s);
+    launch_rowsum(1, np, F(L.dlogit), np, nullptr, G.b_g2, s);
+    launch_colsum(n, d, F(L.dxe), d, nullptr, 0, nullptr, 1, F(L.part), G.q_ln_b, s);
+    launch_colsum(n, d, F(L.dxe), d, F(L.xhat), d, nullptr, 1, F(L.part), G.q_ln_g, s);
+    launch_colsum(n, d, F(L.dxe), d, nullptr, 0, a.depth, nd, F(L.part), G.E_dep, s);
+    if (rms_w != nullptr) launch_colsum(n, d, a.dh_hat, d, F(L.hn), d, nullptr, 1, F(L.part), G.rms_w, s);
+  }
+  FOVEA_HIP(hipGetLastError());
+  return FOVEA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -742,6 +1025,96 @@ fovea_status fovea_lm_topk(fovea_ctx* c, int32_t n_rows, const void* h, const vo
   uint64_t* cand = static_cast<uint64_t*>(workspace);
   return c->bf16 ? run_lm_topk<bf16_t>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream)
                  : run_lm_topk<float>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream);
+}
+
+size_t fovea_retrieve_fuse_backward_workspace(const fovea_ctx* c, int32_t B, int32_t n_nodes_total,
+                                              int32_t k_max) {
+  if (c == nullptr || B < 0 || n_nodes_total < 0 || k_max < 1 || k_max > kMaxKmax) return 0;
+  return bwd_layout(c->dims, B, n_nodes_total, k_max).total;
+}
+
+fovea_status fovea_retrieve_fuse_backward(
+    fovea_ctx* c, const fovea_params* p, int32_t B, const int64_t* mem_off, int64_t n_mem_total,
+    int32_t m_max, const float* keys, const float* values, const int32_t* node_off,
+    int32_t n_nodes_total, int32_t t_max, const float* h, const int32_t* depth, const int32_t* K,
+    const int32_t* idx, int32_t k_max, const float* dh_hat, float* dh, float* dkeys,
+    float* dvalues, const fovea_grads* g, void* workspace, size_t workspace_bytes,
+    hipStream_t stream) {
+  if (c == nullptr || p == nullptr || g == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (c->bf16) return FOVEA_ERR_UNSUPPORTED;
+  if (B < 0 || n_mem_total < 0 || m_max < 0 || n_nodes_total < 0 || t_max < 0 || k_max < 1)
+    return FOVEA_ERR_INVALID_ARG;
+  if (n_nodes_total > 0 && (B == 0 || t_max == 0)) return FOVEA_ERR_INVALID_ARG;
+  if (m_max > kMaxM || k_max > kMaxKmax || n_mem_total > (int64_t{1} << 40)) return FOVEA_ERR_UNSUPPORTED;
+  if ((2 * static_cast<size_t>(c->dims.d_m) + k_max) * 4 > 150 * 1024) return FOVEA_ERR_UNSUPPORTED;
+  const void* wreq[] = {p->q_ln_g, p->q_ln_b, p->E_dep, p->W_Q, p->W_c1, p->b_c1,
+                        p->W_c2,   p->b_c2,   p->W_g1,  p->b_g1, p->w_g2};
+  for (const void* r : wreq)
+    if (r == nullptr) return FOVEA_ERR_INVALID_ARG;
+  float* greq[] = {g->W_Q, g->q_ln_g, g->q_ln_b, g->E_dep, g->W_c1, g->b_c1, g->W_c2,
+                   g->b_c2, g->W_g1, g->b_g1, g->w_g2, g->b_g2};
+  for (float* r : greq)
+    if (r == nullptr || !aligned16(r)) return FOVEA_ERR_INVALID_ARG;
+  if ((p->rms_w != nullptr) != (g->rms_w != nullptr)) return FOVEA_ERR_INVALID_ARG;
+  if (std::isnan(p->b_g2)) return FOVEA_ERR_INVALID_ARG;
+  if (mem_off == nullptr || node_off == nullptr || workspace == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (n_nodes_total > 0 && dh == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (n_mem_total > 0 && (dkeys == nullptr || dvalues == nullptr)) return FOVEA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return FOVEA_ERR_WORKSPACE;
+  const BwdLayout L = bwd_layout(c->dims, B, n_nodes_total, k_max);
+  if (workspace_bytes < L.total) return FOVEA_ERR_WORKSPACE;
+  const fovea_dims& D = c->dims;
+  if (n_nodes_total == 0) {
+    // no node: every gradient is zero
+    const int64_t sizes[] = {int64_t{D.d_m} * D.d, D.d, D.d, int64_t{D.n_depth} * D.d,
+                             int64_t{D.d_c} * (D.d + D.d_m), D.d_c, int64_t{D.d} * D.d_c, D.d,
+                             int64_t{D.d_c} * (D.d + D.d_m), D.d_c, D.d_c, 1};
+    for (int i = 0; i < 12; ++i) launch_fill(greq[i], sizes[i], stream);
+    if (g->rms_w) launch_fill(g->rms_w, D.d, stream);
+    launch_fill(dkeys, n_mem_total * D.d_m, stream);
+    launch_fill(dvalues, n_mem_total * D.d_m, stream);
+    return hipGetLastError() == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+  }
+  if (h == nullptr || depth == nullptr || K == nullptr || idx == nullptr || dh_hat == nullptr)
+    return FOVEA_ERR_INVALID_ARG;
+  if (n_mem_total > 0 && (keys == nullptr || values == nullptr)) return FOVEA_ERR_INVALID_ARG;
+  if (!aligned16(h) || !aligned16(dh_hat) || !aligned16(dh) || !aligned16(keys) ||
+      !aligned16(values) || !aligned16(dkeys) || !aligned16(dvalues))
+    return FOVEA_ERR_INVALID_ARG;
+  const size_t nh = static_cast<size_t>(n_nodes_total) * D.d * 4;
+  const size_t nk = static_cast<size_t>(n_mem_total) * D.d_m * 4;
+  if (overlaps(dh, nh, h, nh) || overlaps(dh, nh, dh_hat, nh) || overlaps(dh, nh, workspace, L.total) ||
+      overlaps(dkeys, nk, keys, nk) || overlaps(dkeys, nk, values, nk) ||
+      overlaps(dvalues, nk, keys, nk) || overlaps(dvalues, nk, values, nk) ||
+      overlaps(dkeys, nk, dvalues, nk) || overlaps(dkeys, nk, workspace, L.total) ||
+      overlaps(dvalues, nk, workspace, L.total))
+    return FOVEA_ERR_INVALID_ARG;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
+  BwdArgs a;
+  a.P = p;
+  a.B = B;
+  a.mem_off = mem_off;
+  a.n_mem = n_mem_total;
+  a.m_max = m_max;
+  a.keys = keys;
+  a.values = values;
+  a.node_off = node_off;
+  a.n = n_nodes_total;
+  a.t_max = t_max;
+  a.h = h;
+  a.depth = depth;
+  a.K = K;
+  a.idx = idx;
+  a.k_max = k_max;
+  a.dh_hat = dh_hat;
+  a.dh = dh;
+  a.dkeys = dkeys;
+  a.dvalues = dvalues;
+  a.G = g;
+  a.ws = static_cast<char*>(workspace);
+  return run_backward(c, a, stream);
 }
 
 }  // extern "C"

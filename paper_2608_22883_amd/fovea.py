@@ -29,6 +29,7 @@ FOVEA_DATA_BAD_NODE_OFFSETS = 0x1
 FOVEA_DATA_BAD_MEM_OFFSETS = 0x2
 FOVEA_DATA_BAD_DEPTH = 0x4
 FOVEA_DATA_BAD_TAU = 0x8
+FOVEA_DATA_BAD_SELECTION = 0x10
 
 FOVEA_MAX_M = 16384
 FOVEA_MAX_KMAX = 1024
@@ -40,7 +41,7 @@ EXPORTED = [
     "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
     "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
     "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
-    "fovea_lm_topk",
+    "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward",
 ]
 
 
@@ -63,6 +64,14 @@ PARAM_TENSORS = ["mem_ln_g", "mem_ln_b", "W_K", "W_U", "q_ln_g", "q_ln_b", "E_de
 class Params(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in PARAM_TENSORS] + [
         ("b_g2", ctypes.c_float), ("rms_w", ctypes.c_void_p)]
+
+
+GRAD_TENSORS = ["W_Q", "q_ln_g", "q_ln_b", "E_dep", "W_c1", "b_c1", "W_c2", "b_c2", "W_g1",
+                "b_g1", "w_g2", "b_g2", "rms_w"]
+
+
+class Grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in GRAD_TENSORS]
 
 
 def _load() -> ctypes.CDLL:
@@ -93,6 +102,12 @@ def _load() -> ctypes.CDLL:
     lib.fovea_profile_read.restype = i32
     lib.fovea_profile_read.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_char_p),
                                        ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
+    lib.fovea_retrieve_fuse_backward_workspace.restype = sz
+    lib.fovea_retrieve_fuse_backward_workspace.argtypes = [vp, i32, i32, i32]
+    lib.fovea_retrieve_fuse_backward.restype = ctypes.c_int
+    lib.fovea_retrieve_fuse_backward.argtypes = [
+        vp, ctypes.POINTER(Params), i32, vp, i64, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, i32,
+        vp, vp, vp, vp, ctypes.POINTER(Grads), vp, sz, vp]
     lib.fovea_lm_topk_workspace.restype = sz
     lib.fovea_lm_topk_workspace.argtypes = [vp, i32, i32, i32]
     lib.fovea_lm_topk.restype = ctypes.c_int
@@ -202,6 +217,37 @@ def fovea_lm_topk(ctx: int, n_rows: int, h, W_LM, vocab: int, k: int, idx_out, l
     _check(st, "fovea_lm_topk")
 
 
+def fovea_retrieve_fuse_backward_workspace(ctx: int, B: int, n_nodes_total: int, k_max: int) -> int:
+    return lib.fovea_retrieve_fuse_backward_workspace(ctx, B, n_nodes_total, k_max)
+
+
+def fovea_retrieve_fuse_backward(ctx: int, params: dict, b_g2: float, B: int, mem_off,
+                                 n_mem_total: int, m_max: int, keys, values, node_off,
+                                 n_nodes_total: int, t_max: int, h, depth, K, idx, k_max: int,
+                                 dh_hat, dh, dkeys, dvalues, grads: dict, workspace=None,
+                                 stream=None) -> None:
+    """Same arguments as the C entry point; params / grads: dicts of fp32 device tensors
+    named as in PARAM_TENSORS (+ "rms_w") / GRAD_TENSORS."""
+    f32 = torch.float32
+    P = Params()
+    for nme in PARAM_TENSORS:
+        setattr(P, nme, _ptr(params.get(nme), f32, nme))
+    P.b_g2 = float(b_g2)
+    P.rms_w = _ptr(params.get("rms_w"), f32, "rms_w")
+    G = Grads()
+    for nme in GRAD_TENSORS:
+        setattr(G, nme, _ptr(grads.get(nme), f32, "grad " + nme))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.fovea_retrieve_fuse_backward(
+        ctx, ctypes.byref(P), B, _ptr(mem_off, torch.int64, "mem_off"), n_mem_total, m_max,
+        _ptr(keys, f32, "keys"), _ptr(values, f32, "values"), _ptr(node_off, torch.int32, "node_off"),
+        n_nodes_total, t_max, _ptr(h, f32, "h"), _ptr(depth, torch.int32, "depth"),
+        _ptr(K, torch.int32, "K"), _ptr(idx, torch.int32, "idx"), k_max, _ptr(dh_hat, f32, "dh_hat"),
+        _ptr(dh, f32, "dh"), _ptr(dkeys, f32, "dkeys"), _ptr(dvalues, f32, "dvalues"),
+        ctypes.byref(G), _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+    _check(st, "fovea_retrieve_fuse_backward")
+
+
 def fovea_last_error(ctx: int, stream=None) -> tuple[int, int]:
     bits = ctypes.c_uint32(0)
     st = lib.fovea_last_error(ctx, _stream(stream), ctypes.byref(bits))
@@ -252,7 +298,8 @@ class Fovea:
             if v is None:
                 continue
             self.params[n] = torch.as_tensor(v).to(device=self.device, dtype=self.dtype).contiguous()
-        self.ctx = fovea_create(self.dims, self.params, float(weights["b_g2"]), stream)
+        self.b_g2 = float(weights["b_g2"])
+        self.ctx = fovea_create(self.dims, self.params, self.b_g2, stream)
         self.workspace = None
         self.lm_workspace = None
 
@@ -315,3 +362,30 @@ class Fovea:
             self.lm_workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         fovea_lm_topk(self.ctx, n, h, W_LM, vocab, k, idx, logit, self.lm_workspace, stream)
         return idx, logit
+
+    def retrieve_fuse_backward(self, inp: dict, K: torch.Tensor, idx: torch.Tensor,
+                               dh_hat: torch.Tensor, stream=None) -> dict:
+        """Gradients of one step (fp32 context): inp as for retrieve_fuse; K / idx the
+        selection to hold fixed.  Returns dh, dkeys, dvalues and "d<weight>" entries."""
+        dev, f32 = self.device, torch.float32
+        n, d = inp["h"].shape
+        d_m, d_c, nd = self.dims.d_m, self.dims.d_c, self.dims.n_depth
+        shapes = dict(W_Q=(d_m, d), q_ln_g=(d,), q_ln_b=(d,), E_dep=(nd, d), W_c1=(d_c, d + d_m),
+                      b_c1=(d_c,), W_c2=(d, d_c), b_c2=(d,), W_g1=(d_c, d + d_m), b_g1=(d_c,),
+                      w_g2=(d_c,), b_g2=(1,), rms_w=(d,))
+        grads = {k: torch.empty(v, dtype=f32, device=dev) for k, v in shapes.items()
+                 if k != "rms_w" or "rms_w" in self.params}
+        n_mem = inp["keys"].shape[0]
+        dh = torch.empty(n, d, dtype=f32, device=dev)
+        dkeys = torch.empty(n_mem, d_m, dtype=f32, device=dev)
+        dvalues = torch.empty(n_mem, d_m, dtype=f32, device=dev)
+        B = inp["mem_off"].numel() - 1
+        need = fovea_retrieve_fuse_backward_workspace(self.ctx, B, n, idx.shape[1])
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        fovea_retrieve_fuse_backward(
+            self.ctx, self.params, self.b_g2, B, inp["mem_off"], n_mem, inp["m_max"], inp["keys"],
+            inp["values"], inp["node_off"], n, inp["t_max"], inp["h"], inp["depth"], K, idx,
+            idx.shape[1], dh_hat, dh, dkeys, dvalues, grads, ws, stream)
+        out = {"d" + k: v for k, v in grads.items()}
+        out.update(dh=dh, dkeys=dkeys, dvalues=dvalues)
+        return out

@@ -4,4 +4,5 @@ draws random arrays with the shapes and statistics of the paper's workloads and 
 them once to the storage dtype."""
 
 from .workloads import (  # noqa: F401
-    LM_HEADS, WORKLOADS, Case, Workload, make_case, make_lm_case, make_memory_case, make_weights)
+    LM_HEADS, WORKLOADS, Case, Workload, make_case, make_lm_case, make_memory_case, make_output_grad,
+    make_weights)

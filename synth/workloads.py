@@ -289,3 +289,9 @@ def make_lm_case(n: int, d: int, vocab: int, dtype: str, seed: int):
     h = _normal(rng, (n, d), 1.0, dtype)
     W = _normal(rng, (vocab, d), 1.0 / math.sqrt(d), dtype)
     return h, W
+
+
+def make_output_grad(n: int, d: int, seed: int) -> np.ndarray:
+    """dL/dh_hat for the backward: N(0, 1), fp32-exact, returned as float64."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return round_to(rng.standard_normal((n, d)), "f32")
