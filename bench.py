@@ -14,6 +14,9 @@ HIP events after a device synchronisation.  A second, profiled pass brackets eve
 kernel with HIP events for the per-kernel roofline.  The fp64 oracle is timed on the
 host cores on a bounded sample as the CPU baseline.
 
+--backward times fovea_retrieve_fuse_backward (fp32 context, the selection of one
+forward run held fixed, dL/dh_hat synthetic) on the workload's shapes instead.
+
 --lm-head vicuna7b|qwen2_5_7b extends every step by the drafter's LM head over the
 corrected states and the top-K_c (--kc, default 6) candidate extraction
 (fovea_lm_topk), with a synthetic head of that vocabulary; the CPU baseline is then
@@ -56,6 +59,8 @@ def parse():
     ap.add_argument("--lm-head", default=None, choices=["vicuna7b", "qwen2_5_7b"],
                     help="extend the step by the drafter's LM head and top-K_c candidates")
     ap.add_argument("--kc", type=int, default=6, help="candidates per node with --lm-head")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward of the step (fp32) instead of the forward")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
     return ap.parse_args()
@@ -161,6 +166,96 @@ def cpu_baseline(case, budget_s):
                        f"affinity cpus={len(os.sched_getaffinity(0))}")
 
 
+def backward_main(args):
+    """One step = one fovea_retrieve_fuse_backward call over the whole batch (fp32)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_22883_amd as F
+    from synth import WORKLOADS, make_case, make_output_grad
+
+    wl = WORKLOADS[args.workload].with_(dtype="f32")
+    log(f"[bench] generating {wl.name} (fp32) ...")
+    case = make_case(wl)
+    W = case.weights
+    dev = torch.device("cuda:0")
+    dims = dict(d=wl.d, d_v=wl.d, d_m=wl.d_m, d_c=wl.d_c, n_depth=wl.n_depth, dtype=0,
+                ln_eps=W["ln_eps"], rms_eps=W["rms_eps"])
+    fv = F.Fovea(dims, W, device=dev)
+
+    def dev_t(x, d=torch.float32):
+        return torch.tensor(np.asarray(x), dtype=d, device=dev)
+
+    inp = dict(mem_off=torch.tensor(case.mem_off, dtype=torch.int64, device=dev),
+               keys=dev_t(case.keys), values=dev_t(case.values), valid=None,
+               node_off=torch.tensor(case.node_off, dtype=torch.int32, device=dev),
+               h=dev_t(case.h), depth=torch.tensor(case.depth, dtype=torch.int32, device=dev),
+               tau=dev_t(case.tau), m_max=case.m_max, t_max=case.t_max, k_min=case.k_min,
+               k_max=case.k_max)
+    out = fv.retrieve_fuse(inp, debug=True)
+    torch.cuda.synchronize()
+    K, idx = out.k, out.idx
+    n, d, d_m, d_c = case.n_nodes, wl.d, wl.d_m, wl.d_c
+    dh_hat = dev_t(make_output_grad(n, d, wl.seed + 17))
+    grads = fv.retrieve_fuse_backward(inp, K, idx, dh_hat)  # allocates the outputs once
+    dh, dkeys, dvalues = grads.pop("dh"), grads.pop("dkeys"), grads.pop("dvalues")
+    g = {k[1:]: v for k, v in grads.items()}
+    B = wl.B
+    ws = torch.empty(F.fovea_retrieve_fuse_backward_workspace(fv.ctx, B, n, case.k_max),
+                     dtype=torch.uint8, device=dev)
+
+    def step():
+        F.fovea_retrieve_fuse_backward(
+            fv.ctx, fv.params, fv.b_g2, B, inp["mem_off"], inp["keys"].shape[0], case.m_max,
+            inp["keys"], inp["values"], inp["node_off"], n, case.t_max, inp["h"], inp["depth"],
+            K, idx, case.k_max, dh_hat, dh, dkeys, dvalues, g, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"[bench] backward, {args.steps} steps: {ms * 1e3:.1f} us/step")
+    F.fovea_profile(fv.ctx, True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    prof = F.fovea_profile_read(fv.ctx, 32)
+    F.fovea_profile(fv.ctx, False)
+    npad = (n + 63) // 64 * 64
+    gemm_flops = 2 * n * (d * d_m + (d + d_m) * 2 * d_c + d_c * d + d * d_c + 2 * d_c * (d + d_m)
+                          + d_m * d) + 2 * npad * (d * d_c + 2 * d_c * (d + d_m) + d_m * d)
+    kernels = []
+    for name, (tot, cnt) in prof.items():
+        per_step_us = tot / args.steps * 1e3
+        e = dict(name=name, us_per_step=round(per_step_us, 2), timed_regions_per_step=cnt // args.steps)
+        if name == "bwd_gemm":
+            e["TFLOPs"] = round(gemm_flops / (per_step_us * 1e-6) / 1e12, 2)
+        kernels.append(e)
+        log(f"[bench] {name:14s} {per_step_us:9.2f} us/step  ({cnt // args.steps} timed regions)")
+    kernels.sort(key=lambda k: -k["us_per_step"])
+    gk = next(k for k in kernels if k["name"] == "bwd_gemm")
+    line = dict(
+        metric="draft states/sec for the backward of retrieve+fuse (fp32, selection held fixed)",
+        value=round(n / (ms * 1e-3), 1), unit="states/s", n_gpus=1, steps=args.steps,
+        warmup=args.warmup, ms_per_step=round(ms, 5), higher_is_better=True, scaling="weak",
+        vs_baseline=None, dtype="f32", data="synthetic",
+        config=dict(workload=wl.name, mode="backward", B=wl.B, T=wl.T, M=wl.M, d=d, d_m=d_m,
+                    d_c=d_c, k_max=wl.k_max, states_per_step=n),
+        roofline=dict(bound="mfma", achieved=gk["TFLOPs"], peak=PEAK_FP32_TFLOPS, unit="TFLOP/s",
+                      frac=round(gk["TFLOPs"] / PEAK_FP32_TFLOPS, 4), traffic=None,
+                      kernel="bwd_gemm (all GEMM launches of a step)"),
+        kernels=kernels)
+    fv.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -172,6 +267,10 @@ def main():
               "so more GPUs would each run this same single-GPU step on their share of the "
               "requests; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.backward:
+        backward_main(args)
+        return
 
     import numpy as np
     import torch
