@@ -201,7 +201,7 @@ def backward_main(args):
     dh, dkeys, dvalues = grads.pop("dh"), grads.pop("dkeys"), grads.pop("dvalues")
     g = {k[1:]: v for k, v in grads.items()}
     B = wl.B
-    ws = torch.empty(F.fovea_retrieve_fuse_backward_workspace(fv.ctx, B, n, case.k_max),
+    ws = torch.empty(F.fovea_retrieve_fuse_backward_workspace(fv.ctx, B, n, case.m_max, case.k_max),
                      dtype=torch.uint8, device=dev)
 
     def step():

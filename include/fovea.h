@@ -185,7 +185,8 @@ typedef struct {
 
 /* Bytes of workspace fovea_retrieve_fuse_backward needs (0 on bad arguments). */
 size_t fovea_retrieve_fuse_backward_workspace(const fovea_ctx* ctx, int32_t B,
-                                              int32_t n_nodes_total, int32_t k_max);
+                                              int32_t n_nodes_total, int32_t m_max,
+                                              int32_t k_max);
 
 /* Backward of one draft step, for training the module (Method, training objective;
  * appendix, draft model training, where the retrieval cardinality is held at K_r = 16):
@@ -197,12 +198,13 @@ size_t fovea_retrieve_fuse_backward_workspace(const fovea_ctx* ctx, int32_t B,
  *            (the memory-build weights are not read); b_g2 and rms_w as there.
  *   B, mem_off, n_mem_total, m_max, keys, values, node_off, n_nodes_total, t_max, h,
  *   depth    as for fovea_retrieve_fuse (fp32 arrays).
- *   K        [n_nodes_total] int32, idx [n_nodes_total, k_max] int32: the selection.
+ *   K        [n_nodes_total] int32, idx [n_nodes_total, k_max] int32: the selection
+ *            (a node's first K indices must be distinct, as the forward writes them).
  *   dh_hat   [n_nodes_total, d] fp32: dL/dh_hat.
  * Outputs (fp32 device arrays, overwritten):
  *   dh       [n_nodes_total, d]   dL/dh (through the retrieval and the correction).
- *   dkeys, dvalues [n_mem_total, d_m]: dL/dk_i, dL/du_i (zero for unselected rows;
- *            accumulated with atomic adds, so their last bits may vary between runs).
+ *   dkeys, dvalues [n_mem_total, d_m]: dL/dk_i, dL/du_i (zero for unselected rows).
+ * Every output is deterministic (fixed summation orders).
  *   grads    the weight gradients (see fovea_grads).
  * Nodes that fail validation (offsets, depth, selection) contribute nothing, get a NaN
  * dh row and set sticky bits read by fovea_last_error.  workspace: at least

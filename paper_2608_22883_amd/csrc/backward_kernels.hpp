@@ -18,8 +18,9 @@
 //   query (GEMM) and LayerNorm       dxe = dq W_Q, dh += LN backward of dxe g_q
 //   weight gradients (GEMMs over the node axis of transposed activations) and
 //   bias / gain / E_dep gradients (column sums, deterministic two-stage).
-// The scatter into dkeys / dvalues uses fp32 atomic adds (their order, and so the last
-// bits of those two outputs, can vary between runs); everything else is deterministic.
+// The memory gradients are accumulated per request in a fixed order (dense rows of
+// alpha and ds over the request's memory, then one pass over the request's nodes per
+// tile of memory rows), so every output is deterministic.
 #pragma once
 
 #include "common.hpp"
@@ -45,6 +46,24 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
   return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// sum_{i < K} w[i] * rows[(m0 + ix[i]) * ld + j], the row loads issued eight at a time
+// so that their latencies overlap
+__device__ __forceinline__ float weighted_rows(const float* __restrict__ w, const int32_t* __restrict__ ix,
+                                               int K, const float* __restrict__ rows, int64_t m0,
+                                               int64_t ld, int j) {
+  float acc = 0.f;
+  for (int i0 = 0; i0 < K; i0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = i0 + u < K ? rows[(m0 + ix[i0 + u]) * ld + j] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (i0 + u < K) acc = fmaf(w[i0 + u], v[u], acc);
+  }
+  return acc;
 }
 
 __global__ __launch_bounds__(256) void fill_f32_kernel(int64_t count, float* __restrict__ p, float v) {
@@ -91,6 +110,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(int n, int d, int d_m,
   const int l = min(max(depth[row], 0), n_depth - 1);
   const float* hr = h + static_cast<int64_t>(row) * d;
   const float* er = E_dep + static_cast<int64_t>(l) * d;
+  #pragma unroll 8
   for (int j = threadIdx.x; j < d; j += 256) {
     const float x = ok ? (hr[j] - st.x) * st.y : 0.f;
     xhat[static_cast<int64_t>(row) * d + j] = x;
@@ -142,6 +162,7 @@ __global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m,
   }
   if (tid == 0) ok_out[row] = ok ? 1 : 0;
   if (!ok) K = 0;
+  #pragma unroll 8
   for (int j = tid; j < d_m; j += 256) sq[j] = q[static_cast<int64_t>(row) * d_m + j];
   __syncthreads();
   // scores of the selected entries, one wave per entry
@@ -149,6 +170,7 @@ __global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m,
     const int64_t kr = ni.m0 + idx[static_cast<int64_t>(row) * k_max + i];
     const float* kp = keys + kr * d_m;
     float s = 0.f;
+    #pragma unroll 8
     for (int j = lane; j < d_m; j += 64) s = fmaf(sq[j], kp[j], s);
     s = wave_sum_f32(s);
     if (lane == 0) sa[i] = s * scale;
@@ -171,12 +193,10 @@ __global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m,
   }
   __syncthreads();
   // r = sum alpha_i u_i, columns over the threads
-  for (int j = tid; j < d_m; j += 256) {
-    float r = 0.f;
-    for (int i = 0; i < K; ++i)
-      r = fmaf(sa[i], values[(ni.m0 + idx[static_cast<int64_t>(row) * k_max + i]) * d_m + j], r);
-    y[static_cast<int64_t>(row) * (d + d_m) + d + j] = r;
-  }
+  const int32_t* ixr = idx + static_cast<int64_t>(row) * k_max;
+  #pragma unroll 8
+  for (int j = tid; j < d_m; j += 256)
+    y[static_cast<int64_t>(row) * (d + d_m) + d + j] = weighted_rows(sa, ixr, K, values, ni.m0, d_m, j);
 }
 
 // Per node: gate, h' = h + g c, RMSNorm backward, the residual split and the gate's
@@ -202,11 +222,13 @@ __global__ __launch_bounds__(256) void bwd_rms_gate_kernel(int n, int d, int d_c
   const int64_t ro = static_cast<int64_t>(row) * d;
   const int64_t zo = static_cast<int64_t>(row) * 2 * d_c;
   float t = 0.f;
+  #pragma unroll 8
   for (int j = tid; j < d_c; j += 256) t = fmaf(a[zo + d_c + j], w_g2[j], t);
   const float g = sigmoid_f(block_sum256(t, red) + b_g2);
   float rho = 1.f, tw = 0.f;
   if (rms_w != nullptr) {
     float ss = 0.f, sw = 0.f;
+    #pragma unroll 8
     for (int j = tid; j < d; j += 256) {
       const float hp = fmaf(g, c[ro + j], h[ro + j]);
       ss = fmaf(hp, hp, ss);
@@ -218,6 +240,7 @@ __global__ __launch_bounds__(256) void bwd_rms_gate_kernel(int n, int d, int d_c
   }
   const float k3 = rho * rho * rho * tw / static_cast<float>(d);
   float sdg = 0.f;
+  #pragma unroll 8
   for (int j = tid; j < d; j += 256) {
     const float hp = fmaf(g, c[ro + j], h[ro + j]);
     float dhp;
@@ -234,42 +257,48 @@ __global__ __launch_bounds__(256) void bwd_rms_gate_kernel(int n, int d, int d_c
   }
   const float dl = block_sum256(sdg, red) * g * (1.0f - g);
   if (tid == 0) dlogit[row] = dl;
+  #pragma unroll 8
   for (int j = tid; j < d_c; j += 256) dz[zo + d_c + j] = dl * w_g2[j] * dsilu_f(z[zo + d_c + j]);
 }
 
-// Per node: the readout and score backward.  dr [n, d_m]; writes dq [n, d_m] and adds
-// alpha_i dr into dvalues and ds_i q / sqrt(d_m) into dkeys (atomic, fp32).
-__global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
+// Per node: the readout and score backward.  dr [n, d_m]; writes dq [n, d_m] and the
+// node's dense rows over its request's memory (m_max wide): wa = alpha_i and
+// ws = ds_i / sqrt(d_m) at the selected entries, 0 elsewhere (the selected indices are
+// distinct, as the forward produces them).
+__global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max, int m_max,
                                                       const NodeInfo* __restrict__ info,
                                                       const int32_t* __restrict__ K_in,
                                                       const int32_t* __restrict__ idx,
                                                       const int32_t* __restrict__ ok_in,
                                                       const float* __restrict__ alpha,
-                                                      const float* __restrict__ q,
                                                       const float* __restrict__ dr,
                                                       const float* __restrict__ keys,
                                                       const float* __restrict__ values,
                                                       float scale, float* __restrict__ dq,
-                                                      float* __restrict__ dkeys,
-                                                      float* __restrict__ dvalues) {
+                                                      float* __restrict__ wa,
+                                                      float* __restrict__ ws) {
   extern __shared__ float smem_f[];
-  float* sdr = smem_f;            // dr_n [d_m]
-  float* sq = smem_f + d_m;       // q_n [d_m]
-  float* sds = smem_f + 2 * d_m;  // da, then ds [k_max]
+  float* sdr = smem_f;        // dr_n [d_m]
+  float* sds = smem_f + d_m;  // da, then ds [k_max]
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int K = ok_in[row] ? K_in[row] : 0;
   const int64_t m0 = info[row].m0;
   const int32_t* ix = idx + static_cast<int64_t>(row) * k_max;
   const float* al = alpha + static_cast<int64_t>(row) * k_max;
-  for (int j = tid; j < d_m; j += 256) {
-    sdr[j] = dr[static_cast<int64_t>(row) * d_m + j];
-    sq[j] = q[static_cast<int64_t>(row) * d_m + j];
+  float* war = wa + static_cast<int64_t>(row) * m_max;
+  float* wsr = ws + static_cast<int64_t>(row) * m_max;
+  for (int i = tid; i < m_max; i += 256) {
+    war[i] = 0.f;
+    wsr[i] = 0.f;
   }
+  #pragma unroll 8
+  for (int j = tid; j < d_m; j += 256) sdr[j] = dr[static_cast<int64_t>(row) * d_m + j];
   __syncthreads();
   for (int i = wave; i < K; i += 4) {
     const float* up = values + (m0 + ix[i]) * d_m;
     float s = 0.f;
+    #pragma unroll 8
     for (int j = lane; j < d_m; j += 64) s = fmaf(sdr[j], up[j], s);
     s = wave_sum_f32(s);
     if (lane == 0) sds[i] = s;
@@ -278,19 +307,77 @@ __global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
   float ad = 0.f;
   for (int i = tid; i < K; i += 256) ad = fmaf(al[i], sds[i], ad);
   ad = block_sum256(ad, red);
-  for (int i = tid; i < K; i += 256) sds[i] = al[i] * (sds[i] - ad);
-  __syncthreads();
-  for (int j = tid; j < d_m; j += 256) {
-    float acc = 0.f;
-    const float drj = sdr[j], qj = sq[j] * scale;
-    for (int i = 0; i < K; ++i) {
-      const int64_t mr = (m0 + ix[i]) * d_m + j;
-      acc = fmaf(sds[i], keys[mr], acc);
-      atomicAdd(dvalues + mr, al[i] * drj);
-      atomicAdd(dkeys + mr, sds[i] * qj);
-    }
-    dq[static_cast<int64_t>(row) * d_m + j] = acc * scale;
+  for (int i = tid; i < K; i += 256) {
+    const float dsi = al[i] * (sds[i] - ad);
+    sds[i] = dsi;
+    war[ix[i]] = al[i];  // after the zeroing above (block barrier in block_sum256)
+    wsr[ix[i]] = dsi * scale;
   }
+  __syncthreads();
+  #pragma unroll 8
+  for (int j = tid; j < d_m; j += 256)
+    dq[static_cast<int64_t>(row) * d_m + j] = weighted_rows(sds, ix, K, keys, m0, d_m, j) * scale;
+}
+
+// Memory gradients of one request, one tile of 32 memory rows x 256 columns per block:
+//   dvalues[m0 + i] = sum over the request's nodes t of wa[t][i] dr[t]
+//   dkeys[m0 + i]   = sum over the request's nodes t of ws[t][i] q[t]
+// in node order.  Grid: (ceil(d_m / 256), ceil(m_max / 32), B).
+constexpr int kMemRows = 32;
+
+__global__ __launch_bounds__(256) void bwd_mem_grad_kernel(int d_m, int m_max, int t_max,
+                                                           const int64_t* __restrict__ mem_off,
+                                                           const int32_t* __restrict__ node_off,
+                                                           int n, int64_t n_mem,
+                                                           const float* __restrict__ wa,
+                                                           const float* __restrict__ ws,
+                                                           const float* __restrict__ dr,
+                                                           const float* __restrict__ q,
+                                                           float* __restrict__ dkeys,
+                                                           float* __restrict__ dvalues) {
+  extern __shared__ float smem_f[];  // [t_max][kMemRows] of wa, then of ws
+  float* swa = smem_f;
+  float* sws = smem_f + t_max * kMemRows;
+  const int b = blockIdx.z, r0 = blockIdx.y * kMemRows;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  const int64_t m0 = mem_off[b], m1 = mem_off[b + 1];
+  const int t0 = node_off[b], t1 = node_off[b + 1];
+  // offsets were validated per node; a request whose range is unusable is skipped here
+  const bool ok = 0 <= m0 && m0 <= m1 && m1 <= n_mem && m1 - m0 <= m_max && 0 <= t0 &&
+                  t0 <= t1 && t1 <= n && t1 - t0 <= t_max;
+  const int M = ok ? static_cast<int>(m1 - m0) : 0;
+  if (r0 >= M) return;
+  const int T = t1 - t0;
+  for (int e = threadIdx.x; e < T * kMemRows; e += 256) {
+    const int t = e / kMemRows, r = e % kMemRows;
+    const int64_t src = static_cast<int64_t>(t0 + t) * m_max + min(r0 + r, m_max - 1);
+    swa[e] = wa[src];
+    sws[e] = ws[src];
+  }
+  __syncthreads();
+  if (j >= d_m) return;
+  float au[kMemRows], ak[kMemRows];
+#pragma unroll
+  for (int r = 0; r < kMemRows; ++r) {
+    au[r] = 0.f;
+    ak[r] = 0.f;
+  }
+#pragma unroll 4
+  for (int t = 0; t < T; ++t) {
+    const float drj = dr[static_cast<int64_t>(t0 + t) * d_m + j];
+    const float qj = q[static_cast<int64_t>(t0 + t) * d_m + j];
+#pragma unroll
+    for (int r = 0; r < kMemRows; ++r) {
+      au[r] = fmaf(swa[t * kMemRows + r], drj, au[r]);
+      ak[r] = fmaf(sws[t * kMemRows + r], qj, ak[r]);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kMemRows; ++r)
+    if (r0 + r < M) {
+      dvalues[(m0 + r0 + r) * d_m + j] = au[r];
+      dkeys[(m0 + r0 + r) * d_m + j] = ak[r];
+    }
 }
 
 // Per node: dh += LayerNorm backward of dxe g_q (xhat, rstd); rows of nodes with
@@ -305,6 +392,7 @@ __global__ __launch_bounds__(256) void bwd_ln_kernel(int n, int d, const float* 
   const int row = blockIdx.x, tid = threadIdx.x;
   const int64_t ro = static_cast<int64_t>(row) * d;
   float s1 = 0.f, s2 = 0.f;
+  #pragma unroll 8
   for (int j = tid; j < d; j += 256) {
     const float t = dxe[ro + j] * g_q[j];
     s1 += t;
@@ -314,6 +402,7 @@ __global__ __launch_bounds__(256) void bwd_ln_kernel(int n, int d, const float* 
   const float m2 = block_sum256(s2, red) / static_cast<float>(d);
   const float rstd = stats[row].y;
   const bool ok = ok_in[row] != 0;
+  #pragma unroll 8
   for (int j = tid; j < d; j += 256) {
     const float t = dxe[ro + j] * g_q[j];
     dh[ro + j] = ok ? dh[ro + j] + rstd * (t - m1 - xhat[ro + j] * m2) : __builtin_nanf("");
@@ -381,6 +470,7 @@ enum BwdEpi : int {
   kEpiZ = 1,      // out = v + bias (pre-activation), out2 = SiLU(out)
   kEpiDsilu = 2,  // out = v * SiLU'(aux)
   kEpiSplit = 3,  // col < split: out[col] += v; else out2[col - split] = v
+  kEpiRows = 4,   // row < split: out[row] = v; else out2[row - split] = v
 };
 
 struct BwdGemm {
@@ -428,6 +518,13 @@ __global__ __launch_bounds__(256) void bwd_gemm_kernel(TileMap tm, BwdGemm g) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[e] = v[e] * dsilu_f(zz[e]);
           store8(g.out + static_cast<int64_t>(row) * g.ldo + col0, o);
+        } else if (EPI == kEpiRows) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = v[e];
+          if (row < g.split)
+            store8(g.out + static_cast<int64_t>(row) * g.ldo + col0, o);
+          else
+            store8(g.out2 + static_cast<int64_t>(row - g.split) * g.ldo2 + col0, o);
         } else {
           if (col0 < g.split) {
             float* p = g.out + static_cast<int64_t>(row) * g.ldo + col0;

@@ -488,13 +488,13 @@ fovea_status run_lm_topk(fovea_ctx* c, int n, const void* h, const void* W, int 
 
 struct BwdLayout {
   int npad;
-  size_t node_req, info, stats, tau0, ok, dlogit;
-  size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe;
-  size_t xeT, yT, aT, dcT, dzT, dqT, WQT, Wc2T, W1T, part;
+  size_t node_req, info, stats, tau0, ok, dlogit, b1;
+  size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe, wa, wsel;
+  size_t xeT, yT, aT, dcT, dzT, dqT, WQT, Wc2T, W1T, W1, part;
   size_t total;
 };
 
-BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max) {
+BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max, int m_max) {
   BwdLayout L;
   const size_t d = D.d, dm = D.d_m, dc = D.d_c, nn = n;
   const size_t np = (nn + 63) / 64 * 64;
@@ -511,6 +511,7 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max) {
   L.tau0 = take(static_cast<size_t>(B) * 4);
   L.ok = take(nn * 4);
   L.dlogit = take(np * 4);
+  L.b1 = take(2 * dc * 4);
   L.xhat = take(nn * d * 4);
   L.xe = take(nn * d * 4);
   L.y = take(nn * (d + dm) * 4);
@@ -525,6 +526,8 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max) {
   L.dr = take(nn * dm * 4);
   L.dq = take(nn * dm * 4);
   L.dxe = take(nn * d * 4);
+  L.wa = take(nn * static_cast<size_t>(m_max) * 4);
+  L.wsel = take(nn * static_cast<size_t>(m_max) * 4);
   L.xeT = take(d * np * 4);
   L.yT = take((d + dm) * np * 4);
   L.aT = take(2 * dc * np * 4);
@@ -534,6 +537,7 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max) {
   L.WQT = take(d * dm * 4);
   L.Wc2T = take(dc * d * 4);
   L.W1T = take((d + dm) * 2 * dc * 4);
+  L.W1 = take(2 * dc * (d + dm) * 4);
   L.part = take(static_cast<size_t>(kColChunks) * kColGroups * std::max(d, 2 * dc) * 4);
   L.total = o;
   return L;
@@ -616,7 +620,7 @@ void launch_rowsum(int rows, int len, const float* X, int64_t ldx, const float* 
 fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   const fovea_dims& D = c->dims;
   const int n = a.n, d = D.d, dm = D.d_m, dc = D.d_c, nd = D.n_depth;
-  const BwdLayout L = bwd_layout(D, a.B, n, a.k_max);
+  const BwdLayout L = bwd_layout(D, a.B, n, a.k_max, a.m_max);
   const int np = L.npad;
   char* w = a.ws;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(w + off); };
@@ -633,7 +637,10 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   const fovea_grads& G = *a.G;
   // per-node kernels keep q, dr and the selection's scores in LDS
   const size_t sm_fwd = static_cast<size_t>(dm + a.k_max) * 4;
-  const size_t sm_bwd = static_cast<size_t>(2 * dm + a.k_max) * 4;
+  const size_t sm_bwd = static_cast<size_t>(dm + a.k_max) * 4;
+  const size_t sm_mem = static_cast<size_t>(a.t_max) * kMemRows * 2 * 4;
+  FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_mem_grad_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_mem)));
   FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_sel_fwd_kernel),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_fwd)));
   FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_sel_kernel),
@@ -645,6 +652,8 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
     launch_fill(a.dkeys, a.n_mem * dm, s);
     launch_fill(a.dvalues, a.n_mem * dm, s);
   }
+  FOVEA_HIP(hipMemcpyAsync(F(L.b1), a.P->b_c1, dc * 4, hipMemcpyDeviceToDevice, s));
+  FOVEA_HIP(hipMemcpyAsync(F(L.b1) + dc, a.P->b_g1, dc * 4, hipMemcpyDeviceToDevice, s));
   {
     ProfScope ps(c, kBwdStats, s);
     hipLaunchKernelGGL(row_stats_kernel<float>, dim3((n + 3) / 4), dim3(256), 0, s, n, a.h, d,
@@ -657,6 +666,9 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
     launch_transpose(d, d, dc, W_c2, dc, F(L.Wc2T), d, s);
     launch_transpose(dc, dc, d + dm, W_c1, d + dm, F(L.W1T), 2 * dc, s);
     launch_transpose(dc, dc, d + dm, W_g1, d + dm, F(L.W1T) + dc, 2 * dc, s);
+    // [W_c1; W_g1] as one operand for the layer-1 recompute: two transposes of the
+    // transposed pack give it back in [2 d_c, d + d_m]
+    launch_transpose(d + dm, d + dm, 2 * dc, F(L.W1T), 2 * dc, F(L.W1), d + dm, s);
   }
   {
     ProfScope ps(c, kBwdPrep, s);
@@ -676,15 +688,11 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   }
   {
     ProfScope ps(c, kBwdGemm, s);
-    BwdGemm g = bwd_gemm(n, dc, d + dm, F(L.y), d + dm, W_c1, d + dm, F(L.z), 2 * dc);
-    g.bias = static_cast<const float*>(a.P->b_c1);
+    // layer 1 of both nets in one GEMM (2 d_c columns); the bias is [b_c1; b_g1]
+    BwdGemm g = bwd_gemm(n, 2 * dc, d + dm, F(L.y), d + dm, F(L.W1), d + dm, F(L.z), 2 * dc);
+    g.bias = F(L.b1);
     g.out2 = F(L.a);
     g.ldo2 = 2 * dc;
-    launch_bwd_gemm<kEpiZ>(g, s);
-    g.B = W_g1;
-    g.bias = static_cast<const float*>(a.P->b_g1);
-    g.out = F(L.z) + dc;
-    g.out2 = F(L.a) + dc;
     launch_bwd_gemm<kEpiZ>(g, s);
     BwdGemm g2 = bwd_gemm(n, d, dc, F(L.a), 2 * dc, W_c2, dc, F(L.c), d);
     g2.bias = static_cast<const float*>(a.P->b_c2);
@@ -710,9 +718,13 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   }
   {
     ProfScope ps(c, kBwdSel, s);
-    hipLaunchKernelGGL(bwd_sel_kernel, dim3(n), dim3(256), sm_bwd, s, n, dm, a.k_max, info, a.K, a.idx,
-                       ok, F(L.alpha), F(L.q), F(L.dr), a.keys, a.values, scale, F(L.dq), a.dkeys,
-                       a.dvalues);
+    hipLaunchKernelGGL(bwd_sel_kernel, dim3(n), dim3(256), sm_bwd, s, n, dm, a.k_max, a.m_max, info,
+                       a.K, a.idx, ok, F(L.alpha), F(L.dr), a.keys, a.values, scale, F(L.dq),
+                       F(L.wa), F(L.wsel));
+    if (a.m_max > 0)
+      hipLaunchKernelGGL(bwd_mem_grad_kernel, dim3((dm + 255) / 256, (a.m_max + kMemRows - 1) / kMemRows, a.B),
+                         dim3(256), sm_mem, s, dm, a.m_max, a.t_max, a.mem_off, a.node_off, n, a.n_mem,
+                         F(L.wa), F(L.wsel), F(L.dr), F(L.q), a.dkeys, a.dvalues);
   }
   {
     ProfScope ps(c, kBwdGemm, s);
@@ -735,9 +747,11 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   {
     ProfScope ps(c, kBwdGemm, s);
     launch_bwd_gemm<kEpiStore>(bwd_gemm(d, dc, np, F(L.dcT), np, F(L.aT), np, G.W_c2, dc), s);
-    launch_bwd_gemm<kEpiStore>(bwd_gemm(dc, d + dm, np, F(L.dzT), np, F(L.yT), np, G.W_c1, d + dm), s);
-    launch_bwd_gemm<kEpiStore>(
-        bwd_gemm(dc, d + dm, np, F(L.dzT) + static_cast<int64_t>(dc) * np, np, F(L.yT), np, G.W_g1, d + dm), s);
+    BwdGemm g1 = bwd_gemm(2 * dc, d + dm, np, F(L.dzT), np, F(L.yT), np, G.W_c1, d + dm);
+    g1.split = dc;
+    g1.out2 = G.W_g1;
+    g1.ldo2 = d + dm;
+    launch_bwd_gemm<kEpiRows>(g1, s);
     launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, d, np, F(L.dqT), np, F(L.xeT), np, G.W_Q, d), s);
   }
   {
@@ -1028,9 +1042,11 @@ fovea_status fovea_lm_topk(fovea_ctx* c, int32_t n_rows, const void* h, const vo
 }
 
 size_t fovea_retrieve_fuse_backward_workspace(const fovea_ctx* c, int32_t B, int32_t n_nodes_total,
-                                              int32_t k_max) {
-  if (c == nullptr || B < 0 || n_nodes_total < 0 || k_max < 1 || k_max > kMaxKmax) return 0;
-  return bwd_layout(c->dims, B, n_nodes_total, k_max).total;
+                                              int32_t m_max, int32_t k_max) {
+  if (c == nullptr || B < 0 || n_nodes_total < 0 || m_max < 0 || m_max > kMaxM || k_max < 1 ||
+      k_max > kMaxKmax)
+    return 0;
+  return bwd_layout(c->dims, B, n_nodes_total, k_max, m_max).total;
 }
 
 fovea_status fovea_retrieve_fuse_backward(
@@ -1046,7 +1062,8 @@ fovea_status fovea_retrieve_fuse_backward(
     return FOVEA_ERR_INVALID_ARG;
   if (n_nodes_total > 0 && (B == 0 || t_max == 0)) return FOVEA_ERR_INVALID_ARG;
   if (m_max > kMaxM || k_max > kMaxKmax || n_mem_total > (int64_t{1} << 40)) return FOVEA_ERR_UNSUPPORTED;
-  if ((2 * static_cast<size_t>(c->dims.d_m) + k_max) * 4 > 150 * 1024) return FOVEA_ERR_UNSUPPORTED;
+  if ((static_cast<size_t>(c->dims.d_m) + k_max) * 4 > 150 * 1024) return FOVEA_ERR_UNSUPPORTED;
+  if (static_cast<size_t>(t_max) * kMemRows * 2 * 4 > 150 * 1024) return FOVEA_ERR_UNSUPPORTED;
   const void* wreq[] = {p->q_ln_g, p->q_ln_b, p->E_dep, p->W_Q, p->W_c1, p->b_c1,
                         p->W_c2,   p->b_c2,   p->W_g1,  p->b_g1, p->w_g2};
   for (const void* r : wreq)
@@ -1061,7 +1078,7 @@ fovea_status fovea_retrieve_fuse_backward(
   if (n_nodes_total > 0 && dh == nullptr) return FOVEA_ERR_INVALID_ARG;
   if (n_mem_total > 0 && (dkeys == nullptr || dvalues == nullptr)) return FOVEA_ERR_INVALID_ARG;
   if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return FOVEA_ERR_WORKSPACE;
-  const BwdLayout L = bwd_layout(c->dims, B, n_nodes_total, k_max);
+  const BwdLayout L = bwd_layout(c->dims, B, n_nodes_total, k_max, m_max);
   if (workspace_bytes < L.total) return FOVEA_ERR_WORKSPACE;
   const fovea_dims& D = c->dims;
   if (n_nodes_total == 0) {

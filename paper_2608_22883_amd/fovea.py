@@ -103,7 +103,7 @@ def _load() -> ctypes.CDLL:
     lib.fovea_profile_read.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_char_p),
                                        ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
     lib.fovea_retrieve_fuse_backward_workspace.restype = sz
-    lib.fovea_retrieve_fuse_backward_workspace.argtypes = [vp, i32, i32, i32]
+    lib.fovea_retrieve_fuse_backward_workspace.argtypes = [vp, i32, i32, i32, i32]
     lib.fovea_retrieve_fuse_backward.restype = ctypes.c_int
     lib.fovea_retrieve_fuse_backward.argtypes = [
         vp, ctypes.POINTER(Params), i32, vp, i64, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, i32,
@@ -217,8 +217,9 @@ def fovea_lm_topk(ctx: int, n_rows: int, h, W_LM, vocab: int, k: int, idx_out, l
     _check(st, "fovea_lm_topk")
 
 
-def fovea_retrieve_fuse_backward_workspace(ctx: int, B: int, n_nodes_total: int, k_max: int) -> int:
-    return lib.fovea_retrieve_fuse_backward_workspace(ctx, B, n_nodes_total, k_max)
+def fovea_retrieve_fuse_backward_workspace(ctx: int, B: int, n_nodes_total: int, m_max: int,
+                                           k_max: int) -> int:
+    return lib.fovea_retrieve_fuse_backward_workspace(ctx, B, n_nodes_total, m_max, k_max)
 
 
 def fovea_retrieve_fuse_backward(ctx: int, params: dict, b_g2: float, B: int, mem_off,
@@ -380,7 +381,7 @@ class Fovea:
         dkeys = torch.empty(n_mem, d_m, dtype=f32, device=dev)
         dvalues = torch.empty(n_mem, d_m, dtype=f32, device=dev)
         B = inp["mem_off"].numel() - 1
-        need = fovea_retrieve_fuse_backward_workspace(self.ctx, B, n, idx.shape[1])
+        need = fovea_retrieve_fuse_backward_workspace(self.ctx, B, n, inp["m_max"], idx.shape[1])
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
         fovea_retrieve_fuse_backward(
             self.ctx, self.params, self.b_g2, B, inp["mem_off"], n_mem, inp["m_max"], inp["keys"],

@@ -97,7 +97,7 @@ def test_null_context_paths(lib):
     assert lib.lib.fovea_profile(None, 1) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_profile_read(None, 4, None, None, None) == -1
     assert lib.lib.fovea_lm_topk_workspace(None, 4, 32000, 6) == 0
-    assert lib.lib.fovea_retrieve_fuse_backward_workspace(None, 1, 4, 4) == 0
+    assert lib.lib.fovea_retrieve_fuse_backward_workspace(None, 1, 4, 8, 4) == 0
     assert lib.lib.fovea_retrieve_fuse_backward(
         None, None, 1, None, 0, 0, None, None, None, 0, 0, None, None, None, None, 1, None, None,
         None, None, None, None, 0, None) == lib.FOVEA_ERR_INVALID_ARG

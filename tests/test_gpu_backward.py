@@ -161,7 +161,7 @@ def test_backward_host_errors(lib):
             *out, grads, ws[:1024])
     assert e.value.status == lib.FOVEA_ERR_WORKSPACE
     fv.close()
-    assert lib.fovea_retrieve_fuse_backward_workspace(None, 1, n, case.k_max) == 0
+    assert lib.fovea_retrieve_fuse_backward_workspace(None, 1, n, case.m_max, case.k_max) == 0
 
 
 def test_backward_no_nodes_gives_zero_gradients(lib):
