@@ -28,106 +28,161 @@ __device__ __forceinline__ float sigmoid_f(float x) { return 1.0f / (1.0f + expf
 // partial of the gate logit per row (gate_part[row][tile column], deterministic order;
 // tiles without gate columns write 0).
 template <typename T>
-__global__ __launch_bounds__(256) void corr1_kernel(TileMap tm, int n, const T* __restrict__ rT,
-                                                    int d_m, const T* __restrict__ W1r,
-                                                    const float* __restrict__ P,
-                                                    const float* __restrict__ b1, int d_c,
-                                                    const float* __restrict__ w_g2,
-                                                    T* __restrict__ a_c,
-                                                    float* __restrict__ gate_part) {
+struct Corr1Epi {
+  int n, d_c, N;
+  const float* P;
+  const float* b1;
+  const float* w_g2;
+  T* a_c;
+  __device__ __forceinline__ float operator()(int row, int col0, const float (&v)[8]) const {
+    if (row >= n || col0 >= N) return 0.f;
+    float p[8], b[8], pre[8];
+    load8(P + static_cast<int64_t>(row) * N + col0, p);
+    load8(b1 + col0, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pre[e] = v[e] + p[e] + b[e];
+    if (col0 < d_c) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pre[e] = silu_f(pre[e]);
+      store8(a_c + static_cast<int64_t>(row) * d_c + col0, pre);
+      return 0.f;
+    }
+    float wg[8];
+    load8(w_g2 + (col0 - d_c), wg);
+    float acc_g = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc_g = fmaf(silu_f(pre[e]), wg[e], acc_g);
+    return acc_g;
+  }
+};
+
+struct RowPart {  // part[row][tile] = sum (rows past n dropped)
+  int n, n_tiles, tile;
+  float* part;
+  __device__ __forceinline__ void operator()(int row, float sum) const {
+    if (part != nullptr && row < n) part[static_cast<int64_t>(row) * n_tiles + tile] = sum;
+  }
+};
+
+// ks > 1: split-K (grid.y = ks slices, fp32 partials in part), finished by
+// corr1_combine_kernel with the same epilogue.
+template <typename T>
+__global__ __launch_bounds__(256) void corr1_kernel(TileMap tm, const T* __restrict__ rT, int d_m,
+                                                    const T* __restrict__ W1r, Corr1Epi<T> epi,
+                                                    float* __restrict__ gate_part, int ks,
+                                                    float* __restrict__ part) {
   using C = Corr1Cfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;
   const int m0 = tr * C::BM, n0 = tc * C::BN;
-  const int N = 2 * d_c;
-  const int n_gp = n_parts(N);
+  if (ks > 1) {
+    gemm_splitk_partial<C>(rT, d_m, epi.n, W1r, d_m, epi.N, d_m, ks, m0, n0, part, smem);
+    return;
+  }
   f32x4 acc[C::TM][C::TN];
-  gemm_mainloop<C>(acc, rT, d_m, n, W1r, d_m, N, d_m, m0, n0, smem);
-  gemm_epilogue<C>(
-      acc, smem, m0, n0,
-      [&](int row, int col0, const float(&v)[8]) -> float {
-        if (row >= n || col0 >= N) return 0.f;
-        float p[8], b[8], pre[8];
-        load8(P + static_cast<int64_t>(row) * N + col0, p);
-        load8(b1 + col0, b);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pre[e] = v[e] + p[e] + b[e];
-        if (col0 < d_c) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pre[e] = silu_f(pre[e]);
-          store8(a_c + static_cast<int64_t>(row) * d_c + col0, pre);
-          return 0.f;
-        }
-        float wg[8];
-        load8(w_g2 + (col0 - d_c), wg);
-        float acc_g = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc_g = fmaf(silu_f(pre[e]), wg[e], acc_g);
-        return acc_g;
-      },
-      [&](int row, float sum) {
-        if (row < n) gate_part[static_cast<int64_t>(row) * n_gp + tc] = sum;
-      });
+  gemm_mainloop<C>(acc, rT, d_m, epi.n, W1r, d_m, epi.N, d_m, m0, n0, smem);
+  gemm_epilogue<C>(acc, smem, m0, n0, epi, RowPart{epi.n, n_parts(epi.N), tc, gate_part});
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void corr1_combine_kernel(Corr1Epi<T> epi, float* __restrict__ gate_part,
+                                                            int ks, const float* __restrict__ part) {
+  splitk_combine(epi.n, epi.N, ks, part, epi,
+                 RowPart{epi.n, n_parts(epi.N), static_cast<int>(blockIdx.x), gate_part});
 }
 
 // Layer 2 and the gated residual: c = a_c W_c2^T + b_c2, g = sigmoid(sum(gate_part) + b_g2),
 // h' = h + g c.  Without RMSNorm h' is the output; with it, h' goes to h_out and each
 // block writes the partial sum of h'^2 over its 128 columns (rms_part[row][tile column]).
+// sg holds the gate of rows m0 .. (staged per block).
 template <typename T>
-__global__ __launch_bounds__(256) void corr2_kernel(TileMap tm, int n, const T* __restrict__ a_c,
-                                                    int d_c, const T* __restrict__ Wc2, int d,
-                                                    const float* __restrict__ b_c2,
-                                                    const float* __restrict__ gate_part,
-                                                    float b_g2, const T* __restrict__ h,
-                                                    T* __restrict__ h_out,
-                                                    float* __restrict__ gate_out,
-                                                    float* __restrict__ rms_part, int has_rms) {
+struct Corr2Epi {
+  int n, d;
+  const float* b_c2;
+  const T* h;
+  T* h_out;
+  const float* sg;
+  int m0;
+  __device__ __forceinline__ float operator()(int row, int col0, const float (&v)[8]) const {
+    if (row >= n || col0 >= d) return 0.f;
+    const float g = sg[row - m0];
+    const int64_t o = static_cast<int64_t>(row) * d + col0;
+    float hv[8], b[8], hp[8];
+    load8(h + o, hv);
+    load8(b_c2 + col0, b);
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      hp[e] = fmaf(g, v[e] + b[e], hv[e]);
+      ss = fmaf(hp[e], hp[e], ss);
+    }
+    store8(h_out + o, hp);
+    return ss;
+  }
+};
+
+struct Corr2Args {
+  int d_c;
+  const float* gate_part;
+  float b_g2;
+  float* gate_out;
+  float* rms_part;  // or null without RMSNorm
+};
+
+// gate of `rows` rows from m0 into sg (threads < rows); tile-0 blocks also write gate_out
+__device__ __forceinline__ void stage_gates(const Corr2Args& ca, int n, int m0, int rows, bool first,
+                                            float* sg) {
+  if (threadIdx.x < static_cast<unsigned>(rows)) {
+    const int n_gp = n_parts(2 * ca.d_c);
+    const int row = m0 + threadIdx.x;
+    float g = 0.f;
+    if (row < n) {
+      float sum = 0.f;
+      for (int p2 = 0; p2 < n_gp; ++p2) sum += ca.gate_part[static_cast<int64_t>(row) * n_gp + p2];
+      g = sigmoid_f(sum + ca.b_g2);
+      if (ca.gate_out != nullptr && first) ca.gate_out[row] = g;
+    }
+    sg[threadIdx.x] = g;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void corr2_kernel(TileMap tm, const T* __restrict__ a_c,
+                                                    const T* __restrict__ Wc2, Corr2Epi<T> epi,
+                                                    Corr2Args ca, int ks, float* __restrict__ part) {
   using C = Corr2Cfg<T>;
   static_assert(C::SMEM_BYTES >= C::OUT_BYTES + C::BM * 4, "gate staging");
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;
   const int m0 = tr * C::BM, n0 = tc * C::BN;
-  const int n_gp = n_parts(2 * d_c);
-  const int n_rp = n_parts(d);
+  if (ks > 1) {
+    gemm_splitk_partial<C>(a_c, ca.d_c, epi.n, Wc2, ca.d_c, epi.d, ca.d_c, ks, m0, n0, part, smem);
+    return;
+  }
   f32x4 acc[C::TM][C::TN];
-  gemm_mainloop<C>(acc, a_c, d_c, n, Wc2, d_c, d, d_c, m0, n0, smem);
+  gemm_mainloop<C>(acc, a_c, ca.d_c, epi.n, Wc2, ca.d_c, epi.d, ca.d_c, m0, n0, smem);
   // gate of each row of the tile, next to the epilogue's staging area
   float* sg = reinterpret_cast<float*>(smem + C::OUT_BYTES);
-  if (threadIdx.x < C::BM) {
-    const int row = m0 + threadIdx.x;
-    float g = 0.f;
-    if (row < n) {
-      float sum = 0.f;
-      for (int p2 = 0; p2 < n_gp; ++p2) sum += gate_part[static_cast<int64_t>(row) * n_gp + p2];
-      g = sigmoid_f(sum + b_g2);
-      if (gate_out != nullptr && tc == 0) gate_out[row] = g;
-    }
-    sg[threadIdx.x] = g;
-  }
+  stage_gates(ca, epi.n, m0, C::BM, tc == 0, sg);
   // (the epilogue's first barrier orders these writes before any read)
-  gemm_epilogue<C>(
-      acc, smem, m0, n0,
-      [&](int row, int col0, const float(&v)[8]) -> float {
-        if (row >= n || col0 >= d) return 0.f;
-        const float g = sg[row - m0];
-        const int64_t o = static_cast<int64_t>(row) * d + col0;
-        float hv[8], b[8], hp[8];
-        load8(h + o, hv);
-        load8(b_c2 + col0, b);
-        float ss = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          hp[e] = fmaf(g, v[e] + b[e], hv[e]);
-          ss = fmaf(hp[e], hp[e], ss);
-        }
-        store8(h_out + o, hp);
-        return ss;
-      },
-      [&](int row, float sum) {
-        if (has_rms && row < n) rms_part[static_cast<int64_t>(row) * n_rp + tc] = sum;
-      });
+  epi.sg = sg;
+  epi.m0 = m0;
+  gemm_epilogue<C>(acc, smem, m0, n0, epi, RowPart{epi.n, n_parts(epi.d), tc, ca.rms_part});
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void corr2_combine_kernel(Corr2Epi<T> epi, Corr2Args ca, int ks,
+                                                            const float* __restrict__ part) {
+  __shared__ float sg[16];
+  const int m0 = static_cast<int>(blockIdx.y) * 16;
+  stage_gates(ca, epi.n, m0, 16, blockIdx.x == 0, sg);
+  __syncthreads();
+  epi.sg = sg;
+  epi.m0 = m0;
+  splitk_combine(epi.n, epi.d, ks, part, epi,
+                 RowPart{epi.n, n_parts(epi.d), static_cast<int>(blockIdx.x), ca.rms_part});
 }
 
 // RMSNorm of h' in place: h_out = h' / sqrt(mean(h'^2) + eps) * w, one wave per row,

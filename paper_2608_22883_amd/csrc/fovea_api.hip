@@ -73,8 +73,23 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 // Byte offsets of the retrieve_fuse workspace regions.
 struct WsLayout {
-  size_t node_req, info, stats, q, P, S, rT, a_c, gate_part, rms_part, total;
+  size_t node_req, info, stats, q, P, S, rT, a_c, gate_part, rms_part, splitk, total;
 };
+
+// K slices of the three forward GEMMs (hidden-state GEMM, layer 1, layer 2) at n rows
+struct SplitK {
+  int hq, c1, c2;
+};
+
+SplitK forward_splitk(const fovea_dims& D, int64_t n) {
+  const int bk = D.dtype == FOVEA_BF16 ? 64 : 32;
+  const int ni = static_cast<int>(n);
+  SplitK k;
+  k.hq = splitk_slices(((ni + 127) / 128) * ((D.d_m + 2 * D.d_c + 127) / 128), D.d, bk);
+  k.c1 = splitk_slices(((ni + 63) / 64) * ((2 * D.d_c + 127) / 128), D.d_m, bk);
+  k.c2 = splitk_slices(((ni + 127) / 128) * ((D.d + 127) / 128), D.d_c, bk);
+  return k;
+}
 
 WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
   const size_t es = dm.dtype == FOVEA_BF16 ? 2 : 4;
@@ -90,6 +105,14 @@ WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
   L.a_c = o; o = align_up(o + n * dm.d_c * es);
   L.gate_part = o; o = align_up(o + n * n_parts(2 * dm.d_c) * 4);
   L.rms_part = o; o = align_up(o + n * n_parts(dm.d) * 4);
+  {
+    const SplitK k = forward_splitk(dm, n);
+    size_t need = 0;
+    if (k.hq > 1) need = std::max(need, static_cast<size_t>(k.hq) * n * (dm.d_m + 2 * dm.d_c));
+    if (k.c1 > 1) need = std::max(need, static_cast<size_t>(k.c1) * n * 2 * dm.d_c);
+    if (k.c2 > 1) need = std::max(need, static_cast<size_t>(k.c2) * n * dm.d);
+    L.splitk = o; o = align_up(o + need * 4);
+  }
   L.total = o;
   return L;
 }
@@ -304,6 +327,8 @@ template <typename T>
 fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   const fovea_dims& D = c->dims;
   const WsLayout L = ws_layout(D, a.n, a.m_max);
+  const SplitK ksp = forward_splitk(D, a.n);
+  float* splitk = reinterpret_cast<float*>(a.ws + L.splitk);
   int32_t* node_req = reinterpret_cast<int32_t*>(a.ws + L.node_req);
   NodeInfo* info = reinterpret_cast<NodeInfo*>(a.ws + L.info);
   float2* stats = reinterpret_cast<float2*>(a.ws + L.stats);
@@ -329,10 +354,26 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     const int N = D.d_m + 2 * D.d_c;
     const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (N + C::BN - 1) / C::BN,
                                      static_cast<double>(a.n) * D.d, static_cast<double>(N) * D.d);
+    HqEpi<T> epi;
+    epi.n = a.n;
+    epi.d_m = D.d_m;
+    epi.N = N;
+    epi.n_depth = D.n_depth;
+    epi.n_p = 2 * D.d_c;
+    epi.stats = stats;
+    epi.depth = a.depth;
+    epi.node_req = node_req;
+    epi.c1 = c->q_c1;
+    epi.c2 = c->q_c2;
+    epi.q = q;
+    epi.P = P;
+    const int ks = ksp.hq;
     ProfScope ps(c, kHq, s);
-    hipLaunchKernelGGL(hq_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, a.n, h, D.d,
-                       static_cast<const T*>(c->W_hq), D.d_m, 2 * D.d_c, stats, a.depth, node_req,
-                       D.n_depth, c->q_c1, c->q_c2, q, P);
+    hipLaunchKernelGGL(hq_kernel<T>, dim3(tile_grid(tm), ks), dim3(C::NT), 0, s, tm, a.n, h, D.d,
+                       static_cast<const T*>(c->W_hq), epi, ks, splitk);
+    if (ks > 1)
+      hipLaunchKernelGGL(hq_combine_kernel<T>, dim3((N + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
+                         epi, ks, static_cast<const float*>(splitk));
   }
   // 3. scores for every (node, key) of each request
   if (a.m_max > 0) {
@@ -421,9 +462,20 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     using C = Corr1Cfg<T>;
     const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (2 * D.d_c + C::BN - 1) / C::BN,
                                      static_cast<double>(a.n) * D.d_m, 2.0 * D.d_c * D.d_m);
+    Corr1Epi<T> epi;
+    epi.n = a.n;
+    epi.d_c = D.d_c;
+    epi.N = 2 * D.d_c;
+    epi.P = P;
+    epi.b1 = c->b1;
+    epi.w_g2 = c->w_g2;
+    epi.a_c = a_c;
     ProfScope ps(c, kCorr1, s);
-    hipLaunchKernelGGL(corr1_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, a.n, rT, D.d_m,
-                       static_cast<const T*>(c->W1r), P, c->b1, D.d_c, c->w_g2, a_c, gate_part);
+    hipLaunchKernelGGL(corr1_kernel<T>, dim3(tile_grid(tm), ksp.c1), dim3(C::NT), 0, s, tm, rT, D.d_m,
+                       static_cast<const T*>(c->W1r), epi, gate_part, ksp.c1, splitk);
+    if (ksp.c1 > 1)
+      hipLaunchKernelGGL(corr1_combine_kernel<T>, dim3((epi.N + 127) / 128, (a.n + 15) / 16), dim3(256), 0,
+                         s, epi, gate_part, ksp.c1, static_cast<const float*>(splitk));
   }
   // 6. correction layer 2, gate, residual (+ RMS partials)
   T* h_out = static_cast<T*>(a.h_out);
@@ -431,10 +483,26 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     using C = Corr2Cfg<T>;
     const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (D.d + C::BN - 1) / C::BN,
                                      static_cast<double>(a.n) * D.d_c, static_cast<double>(D.d) * D.d_c);
+    Corr2Epi<T> epi;
+    epi.n = a.n;
+    epi.d = D.d;
+    epi.b_c2 = c->b_c2;
+    epi.h = h;
+    epi.h_out = h_out;
+    epi.sg = nullptr;
+    epi.m0 = 0;
+    Corr2Args ca;
+    ca.d_c = D.d_c;
+    ca.gate_part = gate_part;
+    ca.b_g2 = c->b_g2;
+    ca.gate_out = a.gate_out;
+    ca.rms_part = c->rms_w ? rms_part : nullptr;
     ProfScope ps(c, kCorr2, s);
-    hipLaunchKernelGGL(corr2_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, a.n, a_c, D.d_c,
-                       static_cast<const T*>(c->W_c2), D.d, c->b_c2, gate_part, c->b_g2, h, h_out,
-                       a.gate_out, rms_part, c->rms_w ? 1 : 0);
+    hipLaunchKernelGGL(corr2_kernel<T>, dim3(tile_grid(tm), ksp.c2), dim3(C::NT), 0, s, tm, a_c,
+                       static_cast<const T*>(c->W_c2), epi, ca, ksp.c2, splitk);
+    if (ksp.c2 > 1)
+      hipLaunchKernelGGL(corr2_combine_kernel<T>, dim3((D.d + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
+                         epi, ca, ksp.c2, static_cast<const float*>(splitk));
   }
   // 7. RMSNorm
   if (c->rms_w) {

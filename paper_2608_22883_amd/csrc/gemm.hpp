@@ -385,4 +385,59 @@ struct NoRowSum {
   __device__ __forceinline__ void operator()(int, float) const {}
 };
 
+// Split-K for GEMMs with too few output tiles to fill the chip: block (tile, y) contracts
+// K slice y (Kc = K / ks columns, a multiple of BK) and stores its fp32 partial tile in
+// part[y][M][N]; a combine kernel then sums the slices in order and runs the fused
+// kernel's epilogue (splitk_combine), so the result does not depend on timing.
+template <class C, typename T>
+__device__ __forceinline__ void gemm_splitk_partial(const T* A, int64_t lda, int M, const T* Bw,
+                                                    int64_t ldb, int N, int K, int ks, int m0,
+                                                    int n0, float* __restrict__ part,
+                                                    unsigned char* smem) {
+  const int Kc = K / ks;
+  const int k0 = static_cast<int>(blockIdx.y) * Kc;
+  f32x4 acc[C::TM][C::TN];
+  gemm_mainloop<C>(acc, A + k0, lda, M, Bw + k0, ldb, N, Kc, m0, n0, smem);
+  float* pp = part + static_cast<int64_t>(blockIdx.y) * M * N;
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8]) -> float {
+        if (row < M && col0 < N) store8(pp + static_cast<int64_t>(row) * N + col0, v);
+        return 0.f;
+      },
+      NoRowSum{});
+}
+
+// One block of 256 threads per (16 rows, 128-column tile blockIdx.x): thread t owns
+// columns 8 (t % 16) .. + 7 of row 16 blockIdx.y + t / 16, sums the ks partials in slice
+// order and calls f(row, col0, v) and fr(row, sum over the tile's 128 columns) exactly
+// as gemm_epilogue does (rows and columns past the matrix included: f drops them).
+template <class F, class FR>
+__device__ __forceinline__ void splitk_combine(int M, int N, int ks, const float* __restrict__ part,
+                                               F&& f, FR&& fr) {
+  const int row = static_cast<int>(blockIdx.y) * 16 + static_cast<int>(threadIdx.x >> 4);
+  const int col0 = static_cast<int>(blockIdx.x) * 128 + static_cast<int>(threadIdx.x & 15) * 8;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (row < M && col0 < N) {
+    for (int y = 0; y < ks; ++y) {
+      float t[8];
+      load8(part + (static_cast<int64_t>(y) * M + row) * N + col0, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += t[e];
+    }
+  }
+  float s = f(row, col0, v);
+  s = sum16(s);
+  if ((threadIdx.x & 15) == 0) fr(row, s);
+}
+
+// Number of K slices for a GEMM of `tiles` output tiles: powers of two while the grid
+// stays within one block per compute unit and every slice keeps >= 2 k-tiles.
+inline int splitk_slices(int tiles, int K, int BK) {
+  int ks = 1;
+  if (tiles >= 128) return 1;
+  while (tiles * ks * 2 <= 256 && K % (BK * ks * 2) == 0 && K / (ks * 2) >= 2 * BK) ks *= 2;
+  return ks;
+}
+
 }  // namespace fovea

@@ -207,55 +207,72 @@ using HqCfg = GemmCfg<T, 128, 4>;
 // columns [d_m, d_m + n_p) are h W1h^T, the h half of the correction and gate nets'
 // first layer, kept in fp32 for the layer-1 kernel (P, [n, n_p]).
 template <typename T>
+struct HqEpi {
+  int n, d_m, N, n_depth;
+  int64_t n_p;
+  const float2* stats;
+  const int32_t* depth;
+  const int32_t* node_req;
+  const float* c1;
+  const float* c2;
+  T* q;
+  float* P;
+  __device__ __forceinline__ float operator()(int row, int col0, const float (&v)[8]) const {
+    if (row >= n || col0 >= N) return 0.f;
+    if (col0 >= d_m) {
+      store8(P + static_cast<int64_t>(row) * n_p + (col0 - d_m), v);
+      return 0.f;
+    }
+    const int64_t plane = static_cast<int64_t>(n) * d_m;
+    const float2 st = stats[row];
+    const bool ok = node_req[row] >= 0;
+    const int dep = min(max(depth[row], 0), n_depth - 1);
+    float a[8], b[8], val[8];
+    load8(c1 + col0, a);
+    load8(c2 + static_cast<int64_t>(dep) * d_m + col0, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) val[e] = ok ? st.y * (v[e] - st.x * a[e]) + b[e] : __builtin_nanf("");
+    const int64_t o = static_cast<int64_t>(row) * d_m + col0;
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      float hi[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = bf16_round(val[e]);
+        lo[e] = val[e] - hi[e];
+      }
+      store8(q + o, hi);
+      store8(q + plane + o, lo);
+    } else {
+      store8(q + o, val);
+    }
+    return 0.f;
+  }
+};
+
+// ks > 1: split-K (grid.y = ks slices, fp32 partials in part), finished by
+// hq_combine_kernel with the same epilogue.
+template <typename T>
 __global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __restrict__ h, int d,
-                                                 const T* __restrict__ Whq, int d_m, int n_p,
-                                                 const float2* __restrict__ stats,
-                                                 const int32_t* __restrict__ depth,
-                                                 const int32_t* __restrict__ node_req, int n_depth,
-                                                 const float* __restrict__ c1,
-                                                 const float* __restrict__ c2, T* __restrict__ q,
-                                                 float* __restrict__ P) {
+                                                 const T* __restrict__ Whq, HqEpi<T> epi, int ks,
+                                                 float* __restrict__ part) {
   using C = HqCfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;
   const int m0 = tr * C::BM, n0 = tc * C::BN;
-  const int N = d_m + n_p;
+  if (ks > 1) {
+    gemm_splitk_partial<C>(h, d, n, Whq, d, epi.N, d, ks, m0, n0, part, smem);
+    return;
+  }
   f32x4 acc[C::TM][C::TN];
-  gemm_mainloop<C>(acc, h, d, n, Whq, d, N, d, m0, n0, smem);
-  const int64_t plane = static_cast<int64_t>(n) * d_m;
-  gemm_epilogue<C>(
-      acc, smem, m0, n0,
-      [&](int row, int col0, const float(&v)[8]) -> float {
-        if (row >= n || col0 >= N) return 0.f;
-        if (col0 >= d_m) {
-          store8(P + static_cast<int64_t>(row) * n_p + (col0 - d_m), v);
-          return 0.f;
-        }
-        const float2 st = stats[row];
-        const bool ok = node_req[row] >= 0;
-        const int dep = min(max(depth[row], 0), n_depth - 1);
-        float a[8], b[8], val[8];
-        load8(c1 + col0, a);
-        load8(c2 + static_cast<int64_t>(dep) * d_m + col0, b);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) val[e] = ok ? st.y * (v[e] - st.x * a[e]) + b[e] : __builtin_nanf("");
-        const int64_t o = static_cast<int64_t>(row) * d_m + col0;
-        if constexpr (std::is_same<T, bf16_t>::value) {
-          float hi[8], lo[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            hi[e] = bf16_round(val[e]);
-            lo[e] = val[e] - hi[e];
-          }
-          store8(q + o, hi);
-          store8(q + plane + o, lo);
-        } else {
-          store8(q + o, val);
-        }
-        return 0.f;
-      },
-      NoRowSum{});
+  gemm_mainloop<C>(acc, h, d, n, Whq, d, epi.N, d, m0, n0, smem);
+  gemm_epilogue<C>(acc, smem, m0, n0, epi, NoRowSum{});
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void hq_combine_kernel(HqEpi<T> epi, int ks,
+                                                         const float* __restrict__ part) {
+  splitk_combine(epi.n, epi.N, ks, part, epi, NoRowSum{});
 }
 
 // ---------------------------------------------------------------------------------
