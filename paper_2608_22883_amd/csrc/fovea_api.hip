@@ -281,14 +281,18 @@ struct RFArgs {
   char* ws;
 };
 
-// Keys per score block: 64, 80 or 96, whichever spreads B * tiles blocks over the 256
-// compute units in the fewest waves of work per unit (cost = rounds x keys per block).
+// Keys per score block: 16 kb, kb in {1, 2, 4, 5, 6}, whichever spreads B * tiles blocks
+// over the 256 compute units in the fewest waves of work per unit.  A block streams its
+// keys (32 kb d_m bytes) and its 64 nodes' two q planes (256 d_m bytes), so the work of
+// one block counts as kb + 8 units (few large blocks win at large B, many small blocks
+// at small B).
 int score_keys_per_block(int B, int m_max) {
+  static const int kbs[] = {1, 2, 4, 5, 6};
   int best = 4;
   long best_cost = -1;
-  for (int kb = 4; kb <= 6; ++kb) {
+  for (int kb : kbs) {
     const long blocks = static_cast<long>(B) * ((m_max + 16 * kb - 1) / (16 * kb));
-    const long cost = ((blocks + 255) / 256) * kb;
+    const long cost = ((blocks + 255) / 256) * (kb + 8);
     if (best_cost < 0 || cost < best_cost) {
       best_cost = cost;
       best = kb;
@@ -303,6 +307,8 @@ typedef void (*ScoreKernel)(int, const int64_t*, int64_t, int, const int32_t*, i
 template <int NKC>
 ScoreKernel score_kernel_kb(int kb) {
   switch (kb) {
+    case 1: return score_bf16_kernel<NKC, 1>;
+    case 2: return score_bf16_kernel<NKC, 2>;
     case 5: return score_bf16_kernel<NKC, 5>;
     case 6: return score_bf16_kernel<NKC, 6>;
     default: return score_bf16_kernel<NKC, 4>;
