@@ -19,6 +19,7 @@ Parity status of each function is stated in ``fovea_ref``'s module docstring.
 from .fovea_ref import (  # noqa: F401
     bf16_round,
     build_memory,
+    build_memory_backward,
     correction,
     fold_gain,
     fuse,

@@ -20,7 +20,9 @@ Sources (paper section / equation):
     ``retrieve_fuse_backward`` takes dL/dh_hat and returns the gradients of the states,
     the memory and every per-step weight, by the chain rule through RMSNorm, the gated
     residual, both nets, the renormalised softmax over the selected set and the query;
-    the selected set itself is held fixed (it is a discrete choice).
+    the selected set itself is held fixed (it is a discrete choice);
+    ``build_memory_backward`` carries dL/dkeys and dL/dvalues into W_K, W_U, the
+    memory LayerNorm and the visual tokens.
   * Eq. hidden_correction's z_n = W_LM h_hat_n and Algorithm 1's tree expansion, which
     adds each node's K_c highest-scoring tokens (K_c = 6 in the experimental setup):
     ``lm_topk``.
@@ -72,6 +74,7 @@ __all__ = [
     "fuse",
     "retrieve_fuse",
     "retrieve_fuse_backward",
+    "build_memory_backward",
     "lm_logits",
     "lm_topk",
     "lm_topk_from_logits",
@@ -445,3 +448,27 @@ def retrieve_fuse_backward(W, mem_off, keys, values, node_off, h, depth, idx, K,
                 dq_ln_b=dq_ln_b, dE_dep=dE_dep, dW_c1=dW_c1, db_c1=db_c1, dW_c2=dW_c2,
                 db_c2=db_c2, dW_g1=dW_g1, db_g1=db_g1, dw_g2=dw_g2, db_g2=db_g2,
                 drms_w=drms)
+
+
+def build_memory_backward(V, ln_g, ln_b, W_K, W_U, eps, dkeys, dvalues):
+    """Gradients of the memory build k_i = W_K LN(v_i), u_i = W_U LN(v_i) (Method,
+    image-specific visual memory) given dL/dkeys and dL/dvalues: returns dW_K, dW_U,
+    dmem_ln_g, dmem_ln_b and dV.  fp64, no weight rounding."""
+    f = np.float64
+    V = np.asarray(V, f)
+    g, b = np.asarray(ln_g, f), np.asarray(ln_b, f)
+    W_K, W_U = np.asarray(W_K, f), np.asarray(W_U, f)
+    dk, du = np.asarray(dkeys, f), np.asarray(dvalues, f)
+    mu = V.mean(axis=1, keepdims=True)
+    rstd = 1.0 / np.sqrt(((V - mu) ** 2).mean(axis=1, keepdims=True) + eps)
+    xhat = (V - mu) * rstd
+    xn = xhat * g + b
+    dW_K = dk.T @ xn
+    dW_U = du.T @ xn
+    dxn = dk @ W_K + du @ W_U
+    dg = (dxn * xhat).sum(axis=0)
+    db = dxn.sum(axis=0)
+    dxh = dxn * g
+    dV = rstd * (dxh - dxh.mean(axis=1, keepdims=True)
+                 - xhat * (dxh * xhat).mean(axis=1, keepdims=True))
+    return dict(dW_K=dW_K, dW_U=dW_U, dmem_ln_g=dg, dmem_ln_b=db, dV=dV)

@@ -166,3 +166,46 @@ def test_backward_closed_gate():
     w = torch.tensor(c["W"]["rms_w"])
     (h * torch.rsqrt((h * h).mean(1, keepdim=True) + 1e-6) * w * torch.tensor(c["dh_hat"])).sum().backward()
     np.testing.assert_allclose(G["dh"], h.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def _mem_case(seed=0, n=7, d_v=16, d_m=8):
+    rng = np.random.default_rng(seed)
+    return dict(V=2.0 * rng.standard_normal((n, d_v)) + 0.5,
+                g=1 + 0.2 * rng.standard_normal(d_v), b=0.2 * rng.standard_normal(d_v),
+                W_K=rng.standard_normal((d_m, d_v)) / np.sqrt(d_v),
+                W_U=rng.standard_normal((d_m, d_v)) / np.sqrt(d_v),
+                dk=rng.standard_normal((n, d_m)), du=rng.standard_normal((n, d_m)), eps=1e-5)
+
+
+def _mem_loss(c):
+    k, u = oracle.build_memory(c["V"], c["g"], c["b"], c["W_K"], c["W_U"], c["eps"])
+    return float((c["dk"] * k).sum() + (c["du"] * u).sum())
+
+
+def _mem_grads(c):
+    return oracle.build_memory_backward(c["V"], c["g"], c["b"], c["W_K"], c["W_U"], c["eps"],
+                                        c["dk"], c["du"])
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_memory_backward_matches_finite_differences(seed):
+    c = _mem_case(seed)
+    G = _mem_grads(c)
+    rng = np.random.default_rng(200 + seed)
+    for name, key in (("dV", "V"), ("dW_K", "W_K"), ("dW_U", "W_U"), ("dmem_ln_g", "g"),
+                      ("dmem_ln_b", "b")):
+        x = c[key]
+        ent = _entries(x.shape, rng, 8)
+        np.testing.assert_allclose(G[name][tuple(np.array(ent).T)], _fd(lambda: _mem_loss(c), x, ent),
+                                   rtol=1e-6, atol=1e-8, err_msg=name)
+
+
+def test_memory_backward_matches_torch_autograd():
+    c = _mem_case(3, n=11, d_v=32, d_m=12)
+    t = {k: torch.tensor(c[k], requires_grad=True) for k in ("V", "g", "b", "W_K", "W_U")}
+    x = torch.nn.functional.layer_norm(t["V"], (32,), t["g"], t["b"], c["eps"])
+    ((x @ t["W_K"].T) * torch.tensor(c["dk"]) + (x @ t["W_U"].T) * torch.tensor(c["du"])).sum().backward()
+    G = _mem_grads(c)
+    for name, key in (("dV", "V"), ("dW_K", "W_K"), ("dW_U", "W_U"), ("dmem_ln_g", "g"),
+                      ("dmem_ln_b", "b")):
+        np.testing.assert_allclose(G[name], t[key].grad.numpy(), rtol=1e-10, atol=1e-12, err_msg=name)
