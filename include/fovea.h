@@ -218,6 +218,26 @@ fovea_status fovea_retrieve_fuse_backward(
     const float* dh_hat, float* dh, float* dkeys, float* dvalues, const fovea_grads* grads,
     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of workspace fovea_build_memory_backward needs (0 on bad arguments). */
+size_t fovea_build_memory_backward_workspace(const fovea_ctx* ctx, int64_t n_rows);
+
+/* Backward of the memory build (Method, image-specific visual memory; the module is
+ * trained end to end): given dL/dkeys and dL/dvalues (e.g. from
+ * fovea_retrieve_fuse_backward) for n_rows visual tokens V, the gradients of the
+ * projections and the memory LayerNorm, and optionally of V.  fp32 context and
+ * arithmetic; deterministic.
+ *   params    the raw fp32 weights (W_K, W_U, mem_ln_g, mem_ln_b are read).
+ *   V         [n_rows, d_v]; dkeys, dvalues [n_rows, d_m] (fp32, device).
+ * Outputs (fp32, device, overwritten): dW_K, dW_U [d_m, d_v], dmem_ln_g, dmem_ln_b [d_v],
+ *   dV [n_rows, d_v] or NULL.
+ * workspace: fovea_build_memory_backward_workspace(...) bytes, 256-byte aligned. */
+fovea_status fovea_build_memory_backward(fovea_ctx* ctx, const fovea_params* params,
+                                         int64_t n_rows, const float* V, const float* dkeys,
+                                         const float* dvalues, float* dW_K, float* dW_U,
+                                         float* dmem_ln_g, float* dmem_ln_b, float* dV,
+                                         void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream);
+
 /* Limits of the candidate extraction below. */
 #define FOVEA_LM_MAX_K 16             /* candidates per row */
 #define FOVEA_LM_MAX_VOCAB (1 << 24)  /* vocabulary size */

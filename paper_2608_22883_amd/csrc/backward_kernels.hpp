@@ -381,7 +381,7 @@ __global__ __launch_bounds__(256) void bwd_mem_grad_kernel(int d_m, int m_max, i
 }
 
 // Per node: dh += LayerNorm backward of dxe g_q (xhat, rstd); rows of nodes with
-// ok = 0 become NaN.
+// ok = 0 become NaN (ok_in null: every row is valid).
 __global__ __launch_bounds__(256) void bwd_ln_kernel(int n, int d, const float* __restrict__ dxe,
                                                      const float* __restrict__ xhat,
                                                      const float* __restrict__ g_q,
@@ -401,11 +401,29 @@ __global__ __launch_bounds__(256) void bwd_ln_kernel(int n, int d, const float* 
   const float m1 = block_sum256(s1, red) / static_cast<float>(d);
   const float m2 = block_sum256(s2, red) / static_cast<float>(d);
   const float rstd = stats[row].y;
-  const bool ok = ok_in[row] != 0;
+  const bool ok = ok_in == nullptr || ok_in[row] != 0;
   #pragma unroll 8
   for (int j = tid; j < d; j += 256) {
     const float t = dxe[ro + j] * g_q[j];
     dh[ro + j] = ok ? dh[ro + j] + rstd * (t - m1 - xhat[ro + j] * m2) : __builtin_nanf("");
+  }
+}
+
+// Per row of the memory build's input: xhat = (v - mu) rstd and xn = xhat g + b.
+__global__ __launch_bounds__(256) void ln_apply_kernel(int n, int d, const float* __restrict__ x,
+                                                       const float2* __restrict__ stats,
+                                                       const float* __restrict__ g,
+                                                       const float* __restrict__ b,
+                                                       float* __restrict__ xhat,
+                                                       float* __restrict__ xn) {
+  const int row = blockIdx.x;
+  const float2 st = stats[row];
+  const int64_t ro = static_cast<int64_t>(row) * d;
+#pragma unroll 8
+  for (int j = threadIdx.x; j < d; j += 256) {
+    const float v = (x[ro + j] - st.x) * st.y;
+    xhat[ro + j] = v;
+    xn[ro + j] = fmaf(v, g[j], b[j]);
   }
 }
 

@@ -140,14 +140,14 @@ bool dims_supported(const fovea_dims* d) {
 enum KernelSlot {
   kRowStats, kHq, kScore, kSelect, kCorr1, kCorr2, kRms, kMemStats, kMemProj, kLmHead, kLmMerge,
   kBwdFill, kBwdStats, kBwdTranspose, kBwdPrep, kBwdGemm, kBwdSelFwd, kBwdRmsGate, kBwdSel,
-  kBwdLn, kBwdReduce, kNumSlots
+  kBwdLn, kBwdReduce, kBwdMem, kNumSlots
 };
 const char* const kSlotNames[kNumSlots] = {
     "row_stats",     "hq",           "score",       "select_gather", "corr1",
     "corr2",         "rms",          "mem_row_stats", "mem_proj",    "lm_head",
     "lm_merge",      "bwd_fill",     "bwd_stats",   "bwd_transpose", "bwd_prep",
     "bwd_gemm",      "bwd_sel_fwd",  "bwd_rms_gate", "bwd_sel",      "bwd_ln",
-    "bwd_reduce"};
+    "bwd_reduce",    "bwd_memory"};
 
 hipEvent_t prof_event(fovea_ctx* c) {
   if (!c->prof_pool.empty()) {
@@ -844,6 +844,81 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   return FOVEA_OK;
 }
 
+// memory-build backward: workspace layout and launches
+struct MemBwdLayout {
+  int npad;
+  size_t stats, xhat, xn, dxn, dkT, duT, xnT, WKT, WUT, part, total;
+};
+
+MemBwdLayout mem_bwd_layout(const fovea_dims& D, int64_t n) {
+  MemBwdLayout L;
+  const size_t dv = D.d_v, dm = D.d_m, nn = static_cast<size_t>(n);
+  const size_t np = (nn + 63) / 64 * 64;
+  L.npad = static_cast<int>(np);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  L.stats = take(nn * 8);
+  L.xhat = take(nn * dv * 4);
+  L.xn = take(nn * dv * 4);
+  L.dxn = take(nn * dv * 4);
+  L.dkT = take(dm * np * 4);
+  L.duT = take(dm * np * 4);
+  L.xnT = take(dv * np * 4);
+  L.WKT = take(dv * dm * 4);
+  L.WUT = take(dv * dm * 4);
+  L.part = take(static_cast<size_t>(kColChunks) * kColGroups * dv * 4);
+  L.total = o;
+  return L;
+}
+
+fovea_status run_mem_backward(fovea_ctx* c, const fovea_params* P, int n, const float* V,
+                              const float* dk, const float* du, float* dW_K, float* dW_U,
+                              float* dg, float* db, float* dV, char* w, hipStream_t s) {
+  const fovea_dims& D = c->dims;
+  const int dv = D.d_v, dm = D.d_m;
+  const MemBwdLayout L = mem_bwd_layout(D, n);
+  const int np = L.npad;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(w + off); };
+  float2* stats = reinterpret_cast<float2*>(w + L.stats);
+  const float* W_K = static_cast<const float*>(P->W_K);
+  const float* W_U = static_cast<const float*>(P->W_U);
+  ProfScope ps(c, kBwdMem, s);
+  hipLaunchKernelGGL(row_stats_kernel<float>, dim3((n + 3) / 4), dim3(256), 0, s, n, V, dv, D.ln_eps,
+                     stats, static_cast<const int32_t*>(nullptr), 0, static_cast<const int32_t*>(nullptr),
+                     0, 0, static_cast<const float*>(nullptr), static_cast<const int64_t*>(nullptr),
+                     int64_t{0}, 0, static_cast<int32_t*>(nullptr), static_cast<NodeInfo*>(nullptr), c->err);
+  hipLaunchKernelGGL(ln_apply_kernel, dim3(n), dim3(256), 0, s, n, dv, V, stats,
+                     static_cast<const float*>(P->mem_ln_g), static_cast<const float*>(P->mem_ln_b),
+                     F(L.xhat), F(L.xn));
+  launch_transpose(dm, dm, dv, W_K, dv, F(L.WKT), dm, s);
+  launch_transpose(dm, dm, dv, W_U, dv, F(L.WUT), dm, s);
+  launch_transpose(n, np, dm, dk, dm, F(L.dkT), np, s);
+  launch_transpose(n, np, dm, du, dm, F(L.duT), np, s);
+  launch_transpose(n, np, dv, F(L.xn), dv, F(L.xnT), np, s);
+  // weight gradients over the row axis
+  launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, dv, np, F(L.dkT), np, F(L.xnT), np, dW_K, dv), s);
+  launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, dv, np, F(L.duT), np, F(L.xnT), np, dW_U, dv), s);
+  // dL/dLN(v) = dk W_K + du W_U
+  launch_bwd_gemm<kEpiStore>(bwd_gemm(n, dv, dm, dk, dm, F(L.WKT), dm, F(L.dxn), dv), s);
+  BwdGemm g2 = bwd_gemm(n, dv, dm, du, dm, F(L.WUT), dm, F(L.dxn), dv);
+  g2.split = dv;  // every column accumulates into dxn
+  launch_bwd_gemm<kEpiSplit>(g2, s);
+  launch_colsum(n, dv, F(L.dxn), dv, F(L.xhat), dv, nullptr, 1, F(L.part), dg, s);
+  launch_colsum(n, dv, F(L.dxn), dv, nullptr, 0, nullptr, 1, F(L.part), db, s);
+  if (dV != nullptr) {
+    launch_fill(dV, static_cast<int64_t>(n) * dv, s);
+    hipLaunchKernelGGL(bwd_ln_kernel, dim3(n), dim3(256), 0, s, n, dv, F(L.dxn), F(L.xhat),
+                       static_cast<const float*>(P->mem_ln_g), stats, static_cast<const int32_t*>(nullptr),
+                       dV);
+  }
+  FOVEA_HIP(hipGetLastError());
+  return FOVEA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1206,6 +1281,48 @@ fovea_status fovea_retrieve_fuse_backward(
   a.G = g;
   a.ws = static_cast<char*>(workspace);
   return run_backward(c, a, stream);
+}
+
+size_t fovea_build_memory_backward_workspace(const fovea_ctx* c, int64_t n_rows) {
+  if (c == nullptr || n_rows < 0 || n_rows > (int64_t{1} << 30)) return 0;
+  return mem_bwd_layout(c->dims, n_rows).total;
+}
+
+fovea_status fovea_build_memory_backward(fovea_ctx* c, const fovea_params* p, int64_t n_rows,
+                                         const float* V, const float* dkeys, const float* dvalues,
+                                         float* dW_K, float* dW_U, float* dmem_ln_g,
+                                         float* dmem_ln_b, float* dV, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream) {
+  if (c == nullptr || p == nullptr || n_rows < 0) return FOVEA_ERR_INVALID_ARG;
+  if (c->bf16) return FOVEA_ERR_UNSUPPORTED;
+  if (n_rows > (int64_t{1} << 30)) return FOVEA_ERR_UNSUPPORTED;
+  if (p->W_K == nullptr || p->W_U == nullptr || p->mem_ln_g == nullptr || p->mem_ln_b == nullptr)
+    return FOVEA_ERR_INVALID_ARG;
+  float* outs[] = {dW_K, dW_U, dmem_ln_g, dmem_ln_b};
+  for (float* o : outs)
+    if (o == nullptr || !aligned16(o)) return FOVEA_ERR_INVALID_ARG;
+  const fovea_dims& D = c->dims;
+  if (n_rows == 0) {
+    launch_fill(dW_K, int64_t{D.d_m} * D.d_v, stream);
+    launch_fill(dW_U, int64_t{D.d_m} * D.d_v, stream);
+    launch_fill(dmem_ln_g, D.d_v, stream);
+    launch_fill(dmem_ln_b, D.d_v, stream);
+    return hipGetLastError() == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+  }
+  if (V == nullptr || dkeys == nullptr || dvalues == nullptr || workspace == nullptr)
+    return FOVEA_ERR_INVALID_ARG;
+  if (!aligned16(V) || !aligned16(dkeys) || !aligned16(dvalues) || !aligned16(dV))
+    return FOVEA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return FOVEA_ERR_WORKSPACE;
+  const MemBwdLayout L = mem_bwd_layout(D, n_rows);
+  if (workspace_bytes < L.total) return FOVEA_ERR_WORKSPACE;
+  const size_t nv = static_cast<size_t>(n_rows) * D.d_v * 4;
+  if (overlaps(dV, nv, V, nv) || overlaps(dV, nv, workspace, L.total)) return FOVEA_ERR_INVALID_ARG;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
+  return run_mem_backward(c, p, static_cast<int>(n_rows), V, dkeys, dvalues, dW_K, dW_U, dmem_ln_g,
+                          dmem_ln_b, dV, static_cast<char*>(workspace), stream);
 }
 
 }  // extern "C"

@@ -42,6 +42,7 @@ EXPORTED = [
     "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
     "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
     "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward",
+    "fovea_build_memory_backward_workspace", "fovea_build_memory_backward",
 ]
 
 
@@ -108,6 +109,11 @@ def _load() -> ctypes.CDLL:
     lib.fovea_retrieve_fuse_backward.argtypes = [
         vp, ctypes.POINTER(Params), i32, vp, i64, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, i32,
         vp, vp, vp, vp, ctypes.POINTER(Grads), vp, sz, vp]
+    lib.fovea_build_memory_backward_workspace.restype = sz
+    lib.fovea_build_memory_backward_workspace.argtypes = [vp, i64]
+    lib.fovea_build_memory_backward.restype = ctypes.c_int
+    lib.fovea_build_memory_backward.argtypes = [vp, ctypes.POINTER(Params), i64, vp, vp, vp, vp, vp,
+                                                vp, vp, vp, vp, sz, vp]
     lib.fovea_lm_topk_workspace.restype = sz
     lib.fovea_lm_topk_workspace.argtypes = [vp, i32, i32, i32]
     lib.fovea_lm_topk.restype = ctypes.c_int
@@ -247,6 +253,28 @@ def fovea_retrieve_fuse_backward(ctx: int, params: dict, b_g2: float, B: int, me
         _ptr(dh, f32, "dh"), _ptr(dkeys, f32, "dkeys"), _ptr(dvalues, f32, "dvalues"),
         ctypes.byref(G), _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
     _check(st, "fovea_retrieve_fuse_backward")
+
+
+def fovea_build_memory_backward_workspace(ctx: int, n_rows: int) -> int:
+    return lib.fovea_build_memory_backward_workspace(ctx, n_rows)
+
+
+def fovea_build_memory_backward(ctx: int, params: dict, V, dkeys, dvalues, dW_K, dW_U, dmem_ln_g,
+                                dmem_ln_b, dV=None, workspace=None, stream=None) -> None:
+    """Same arguments as the C entry point; params: dict of fp32 device tensors."""
+    f32 = torch.float32
+    P = Params()
+    for nme in PARAM_TENSORS:
+        setattr(P, nme, _ptr(params.get(nme), f32, nme))
+    P.b_g2 = 0.0
+    P.rms_w = None
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.fovea_build_memory_backward(
+        ctx, ctypes.byref(P), V.shape[0], _ptr(V, f32, "V"), _ptr(dkeys, f32, "dkeys"),
+        _ptr(dvalues, f32, "dvalues"), _ptr(dW_K, f32, "dW_K"), _ptr(dW_U, f32, "dW_U"),
+        _ptr(dmem_ln_g, f32, "dmem_ln_g"), _ptr(dmem_ln_b, f32, "dmem_ln_b"), _ptr(dV, f32, "dV"),
+        _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+    _check(st, "fovea_build_memory_backward")
 
 
 def fovea_last_error(ctx: int, stream=None) -> tuple[int, int]:
@@ -389,4 +417,24 @@ class Fovea:
             idx.shape[1], dh_hat, dh, dkeys, dvalues, grads, ws, stream)
         out = {"d" + k: v for k, v in grads.items()}
         out.update(dh=dh, dkeys=dkeys, dvalues=dvalues)
+        return out
+
+
+    def build_memory_backward(self, V: torch.Tensor, dkeys: torch.Tensor, dvalues: torch.Tensor,
+                              want_dV: bool = True, stream=None) -> dict:
+        """Gradients of the memory build (fp32 context): dW_K, dW_U, dmem_ln_g, dmem_ln_b
+        and (optionally) dV."""
+        dev, f32 = self.device, torch.float32
+        d_m, d_v = self.dims.d_m, self.dims.d_v
+        out = dict(dW_K=torch.empty(d_m, d_v, dtype=f32, device=dev),
+                   dW_U=torch.empty(d_m, d_v, dtype=f32, device=dev),
+                   dmem_ln_g=torch.empty(d_v, dtype=f32, device=dev),
+                   dmem_ln_b=torch.empty(d_v, dtype=f32, device=dev))
+        dV = torch.empty(V.shape[0], d_v, dtype=f32, device=dev) if want_dV else None
+        ws = torch.empty(max(fovea_build_memory_backward_workspace(self.ctx, V.shape[0]), 256),
+                         dtype=torch.uint8, device=dev)
+        fovea_build_memory_backward(self.ctx, self.params, V, dkeys, dvalues, out["dW_K"], out["dW_U"],
+                                    out["dmem_ln_g"], out["dmem_ln_b"], dV, ws, stream)
+        if dV is not None:
+            out["dV"] = dV
         return out

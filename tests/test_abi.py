@@ -29,7 +29,8 @@ def test_header_declares_the_entry_points():
         "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
         "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
         "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
-        "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward"])
+        "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward",
+        "fovea_build_memory_backward_workspace", "fovea_build_memory_backward"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -98,6 +99,9 @@ def test_null_context_paths(lib):
     assert lib.lib.fovea_profile_read(None, 4, None, None, None) == -1
     assert lib.lib.fovea_lm_topk_workspace(None, 4, 32000, 6) == 0
     assert lib.lib.fovea_retrieve_fuse_backward_workspace(None, 1, 4, 8, 4) == 0
+    assert lib.lib.fovea_build_memory_backward_workspace(None, 4) == 0
+    assert lib.lib.fovea_build_memory_backward(None, None, 1, None, None, None, None, None, None,
+                                               None, None, None, 0, None) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_retrieve_fuse_backward(
         None, None, 1, None, 0, 0, None, None, None, 0, 0, None, None, None, None, 1, None, None,
         None, None, None, None, 0, None) == lib.FOVEA_ERR_INVALID_ARG

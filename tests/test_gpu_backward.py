@@ -179,3 +179,29 @@ def test_backward_no_nodes_gives_zero_gradients(lib):
     fv.close()
     for k, v in g.items():
         assert v.numel() == 0 or float(v.abs().max()) == 0.0, k
+
+
+@pytest.mark.parametrize("name,n_rows,affine", [("tiny_f32", 64, "random"), ("llava_b1", 576, "random"),
+                                               ("tiny_f32", 130, "unit")])
+def test_memory_backward_parity(lib, name, n_rows, affine):
+    from synth import make_memory_case
+
+    wl = _wl(name)
+    V, W = make_memory_case(wl, n_rows, affine=affine)
+    dk = make_output_grad(n_rows, wl.d_m, wl.seed + 5)
+    du = make_output_grad(n_rows, wl.d_m, wl.seed + 6)
+    ref = oracle.build_memory_backward(V, W["mem_ln_g"], W["mem_ln_b"], W["W_K"], W["W_U"],
+                                       W["ln_eps"], dk, du)
+    fv = lib.Fovea(dims_of(wl, W, 0), W, device="cuda")
+    t = lambda x: torch.tensor(x, dtype=torch.float32, device="cuda")  # noqa: E731
+    print(f"[gpu] memory backward {name}: rows={n_rows} d_v={wl.d} d_m={wl.d_m}", flush=True)
+    g = fv.build_memory_backward(t(V), t(dk), t(du))
+    torch.cuda.synchronize()
+    st, bits = lib.fovea_last_error(fv.ctx)
+    fv.close()
+    assert st == 0, f"data error bits {bits:#x}"
+    for k in ("dW_K", "dW_U", "dmem_ln_g", "dmem_ln_b", "dV"):
+        r = np.asarray(ref[k])
+        o = g[k].double().cpu().numpy().reshape(r.shape)
+        err = float(np.abs(o - r).max()) / max(float(np.abs(r).max()), 1e-30)
+        assert err <= TOL, f"{k}: max error {err:.2e}"
