@@ -429,9 +429,16 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     const int nch = (D.d_m / VEC + 63) / 64;  // 16-byte chunks per lane per value row
     const bool wave_path = a.k_max <= kWaveSelKmax && a.m_max <= 64 * 64 && nch <= 4;
     if (wave_path) {
-      const dim3 grid(xcd_grid((a.n + 1) / 2)), blk(256);
+      // one node per block when the pairs would leave compute units idle: the gather of a
+      // node then runs on four waves instead of two
+      const bool one = (a.n + 1) / 2 < 256;
+      const dim3 grid(xcd_grid(one ? a.n : (a.n + 1) / 2)), blk(256);
       const int npl = (a.m_max + 63) / 64;
-#define FOVEA_SEL_C(N, C) hipLaunchKernelGGL((select_node_kernel<T, N, C>), grid, blk, 0, s, sa, a.n)
+#define FOVEA_SEL_C(N, C)                                                              \
+  if (one)                                                                             \
+    hipLaunchKernelGGL((select_node_kernel<T, N, C, 1>), grid, blk, 0, s, sa, a.n);    \
+  else                                                                                 \
+    hipLaunchKernelGGL((select_node_kernel<T, N, C, 2>), grid, blk, 0, s, sa, a.n)
 #define FOVEA_SEL(N)              \
   if (nch <= 1) FOVEA_SEL_C(N, 1); \
   else if (nch <= 2) FOVEA_SEL_C(N, 2); \

@@ -1295,29 +1295,35 @@ __device__ __forceinline__ void gather_rows(const T* __restrict__ vbase, int d_m
   }
 }
 
-template <typename T, int NPL, int NCH>
+// NPB nodes per block (2, or 1 for batches with fewer node pairs than compute units):
+// each node's first wave selects; the gather of its K rows is split over the node's
+// 4 / NPB waves (ranks w, w + 4 / NPB, ...) and summed in wave order.
+template <typename T, int NPL, int NCH, int NPB = 2>
 __global__ __launch_bounds__(256) void select_node_kernel(SelectArgs<T> a, int n_nodes) {
+  static_assert(NPB == 1 || NPB == 2, "nodes per block");
   constexpr int VEC = Elem<T>::kPer16B;
   constexpr int NRB = 32 / NCH;  // largest row batch per wave
-  __shared__ unsigned long long cand[2][kWaveSelKmax];
-  __shared__ double pre_s[2][kWaveSelKmax];
-  __shared__ float alpha_s[2][kWaveSelKmax];
-  __shared__ int idx_s[2][kWaveSelKmax];
-  __shared__ __align__(16) float red[2][64 * NCH * VEC];
-  __shared__ int s_K[2];
-  __shared__ int64_t s_m0[2];
+  constexpr int WPN = 4 / NPB;   // waves per node
+  __shared__ unsigned long long cand[NPB][kWaveSelKmax];
+  __shared__ double pre_s[NPB][kWaveSelKmax];
+  __shared__ float alpha_s[NPB][kWaveSelKmax];
+  __shared__ int idx_s[NPB][kWaveSelKmax];
+  __shared__ __align__(16) float red[NPB][WPN - 1][64 * NCH * VEC];
+  __shared__ int s_K[NPB];
+  __shared__ int64_t s_m0[NPB];
 
-  const int pair = xcd_item((n_nodes + 1) / 2);  // a request's nodes share an XCD (and L2)
+  // a request's nodes share an XCD (and L2)
+  const int pair = xcd_item(NPB == 2 ? (n_nodes + 1) / 2 : n_nodes);
   if (pair < 0) return;
   const int lane = threadIdx.x & 63;
-  // waves are renumbered with the block so that the two selecting waves of the blocks
+  // waves are renumbered with the block so that the selecting waves of the blocks
   // resident on a CU fall on different SIMDs (a block's wave w runs on SIMD w)
   const int wave = ((threadIdx.x >> 6) + 2 * ((blockIdx.x >> 3) & 1)) & 3;
-  const int nb = wave & 1;     // the node of the pair this wave works on
-  const int half = wave >> 1;  // 0: selects, then gathers even ranks; 1: odd ranks
+  const int nb = NPB == 2 ? (wave & 1) : 0;     // the node of the block this wave works on
+  const int half = NPB == 2 ? (wave >> 1) : wave;  // 0: selects, then gathers its ranks
   const int cpr = a.d_m / VEC;
   {
-    const int n = 2 * pair + nb;
+    const int n = NPB * pair + nb;
     const bool live = n < n_nodes;
     if (half == 0) {
       uint32_t kv[NPL];
@@ -1350,48 +1356,50 @@ __global__ __launch_bounds__(256) void select_node_kernel(SelectArgs<T> a, int n
       const T* vbase = a.values + s_m0[nb] * a.d_m;
       const int* ix = idx_s[nb];
       const float* al = alpha_s[nb];
-      const int mine = K > half ? (K - half + 1) / 2 : 0;  // ranks half, half + 2, ...
+      const int mine = K > half ? (K - half + WPN - 1) / WPN : 0;  // ranks half, half + WPN, ...
       for (int q0 = 0; q0 < mine;) {
         const int left = mine - q0;
-        const int t0 = half + 2 * q0;
+        const int t0 = half + WPN * q0;
         if (left >= NRB) {
-          gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, NRB, lane, acc);
+          gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, WPN, NRB, lane, acc);
           q0 += NRB;
         } else if (left > NRB / 2) {
-          gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          gather_rows<T, NCH, NRB>(vbase, a.d_m, cpr, ix, al, t0, WPN, left, lane, acc);
           q0 += left;
         } else if (left > NRB / 4) {
-          gather_rows<T, NCH, NRB / 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          gather_rows<T, NCH, NRB / 2>(vbase, a.d_m, cpr, ix, al, t0, WPN, left, lane, acc);
           q0 += left;
         } else if (left > 2) {
-          gather_rows<T, NCH, NRB / 4>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          gather_rows<T, NCH, NRB / 4>(vbase, a.d_m, cpr, ix, al, t0, WPN, left, lane, acc);
           q0 += left;
         } else {
-          gather_rows<T, NCH, 2>(vbase, a.d_m, cpr, ix, al, t0, 2, left, lane, acc);
+          gather_rows<T, NCH, 2>(vbase, a.d_m, cpr, ix, al, t0, WPN, left, lane, acc);
           q0 += left;
         }
       }
     }
-    if (half == 1) {
+    if (half > 0) {
 #pragma unroll
       for (int u = 0; u < NCH; ++u)
 #pragma unroll
         for (int x = 0; x < VEC; x += 4)
-          *reinterpret_cast<f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]) =
+          *reinterpret_cast<f32x4*>(&red[nb][half - 1][(u * 64 + lane) * VEC + x]) =
               f32x4{acc[u][x], acc[u][x + 1], acc[u][x + 2], acc[u][x + 3]};
     }
     __syncthreads();
     if (half == 0 && K >= 0) {  // K < 0: invalid request, outputs already NaN
 #pragma unroll
-      for (int u = 0; u < NCH; ++u)
+      for (int hh = 0; hh < WPN - 1; ++hh)
 #pragma unroll
-        for (int x = 0; x < VEC; x += 4) {
-          const f32x4 p = *reinterpret_cast<const f32x4*>(&red[nb][(u * 64 + lane) * VEC + x]);
-          acc[u][x] += p[0];
-          acc[u][x + 1] += p[1];
-          acc[u][x + 2] += p[2];
-          acc[u][x + 3] += p[3];
-        }
+        for (int u = 0; u < NCH; ++u)
+#pragma unroll
+          for (int x = 0; x < VEC; x += 4) {
+            const f32x4 p = *reinterpret_cast<const f32x4*>(&red[nb][hh][(u * 64 + lane) * VEC + x]);
+            acc[u][x] += p[0];
+            acc[u][x + 1] += p[1];
+            acc[u][x + 2] += p[2];
+            acc[u][x + 3] += p[3];
+          }
       const int64_t rbase = static_cast<int64_t>(n) * a.d_m;
 #pragma unroll
       for (int u = 0; u < NCH; ++u) {
