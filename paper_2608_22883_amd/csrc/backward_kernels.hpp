@@ -481,8 +481,30 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(int cols, int g0, int
   out[static_cast<int64_t>(g0 + g) * cols + j] = acc;
 }
 
-// fp32 GEMM C = A B^T (A [M, K], B [N, K], K a multiple of 32, N a multiple of 8) on the
-// gemm.hpp core, with the epilogues the backward needs.
+// fp32 operands as bf16 planes, for GEMMs on the bf16 matrix cores with close to fp32
+// accuracy: x = hi + lo + O(2^-16 |x|) with hi = bf16(x), lo = bf16(x - hi), and
+//   A B^T = A_hi B_hi^T + A_lo B_hi^T + A_hi B_lo^T + O(2^-16)
+// is one bf16 GEMM over a tripled K with A' = [A_hi | A_lo | A_hi] (pattern 0) and
+// B' = [B_hi | B_hi | B_lo] (pattern 1).  dst [R, 3 C] row-major.
+__global__ __launch_bounds__(256) void split3_kernel(int R, int C, const float* __restrict__ src,
+                                                     int64_t lds, bf16_t* __restrict__ dst,
+                                                     int pattern) {
+  const int64_t total = static_cast<int64_t>(R) * C;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const int r = static_cast<int>(e / C), c = static_cast<int>(e % C);
+    const float x = src[static_cast<int64_t>(r) * lds + c];
+    const float hi = bf16_round(x);
+    const bf16_t bh = f32_to_bf16_bits(hi), bl = f32_to_bf16_bits(x - hi);
+    bf16_t* d = dst + static_cast<int64_t>(r) * 3 * C + c;
+    d[0] = bh;
+    d[C] = pattern == 0 ? bl : bh;
+    d[2 * C] = pattern == 0 ? bh : bl;
+  }
+}
+
+// GEMM C = A B^T (A [M, K], B [N, K], K a multiple of the k-tile, N a multiple of 8) on
+// the gemm.hpp core, fp32 or bf16 operands (fp32 accumulation), with the epilogues the
+// backward needs.
 enum BwdEpi : int {
   kEpiStore = 0,  // out = v (+ bias[col])
   kEpiZ = 1,      // out = v + bias (pre-activation), out2 = SiLU(out)
@@ -493,10 +515,11 @@ enum BwdEpi : int {
 
 struct BwdGemm {
   int M, N, K;
-  const float* A;
+  const void* A;  // fp32, or bf16 planes when bf16
   int64_t lda;
-  const float* B;
+  const void* B;
   int64_t ldb;
+  bool bf16;
   float* out;
   int64_t ldo;
   const float* bias;
@@ -507,15 +530,19 @@ struct BwdGemm {
   int split;
 };
 
-template <int EPI>
+template <typename T>
+using BwdCfg = GemmCfg<T, 64, 4>;
+
+template <int EPI, typename T>
 __global__ __launch_bounds__(256) void bwd_gemm_kernel(TileMap tm, BwdGemm g) {
-  using C = GemmCfg<float, 64, 2>;
+  using C = BwdCfg<T>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;
   const int m0 = tr * C::BM, n0 = tc * C::BN;
   f32x4 acc[C::TM][C::TN];
-  gemm_mainloop<C>(acc, g.A, g.lda, g.M, g.B, g.ldb, g.N, g.K, m0, n0, smem);
+  gemm_mainloop<C>(acc, static_cast<const T*>(g.A), g.lda, g.M, static_cast<const T*>(g.B), g.ldb,
+                   g.N, g.K, m0, n0, smem);
   gemm_epilogue<C>(
       acc, smem, m0, n0,
       [&](int row, int col0, const float(&v)[8]) -> float {

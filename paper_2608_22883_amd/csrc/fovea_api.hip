@@ -571,7 +571,7 @@ struct BwdLayout {
   int npad;
   size_t node_req, info, stats, tau0, ok, dlogit, b1;
   size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe, wa, wsel;
-  size_t xeT, yT, aT, dcT, dzT, dqT, WQT, Wc2T, W1T, W1, part;
+  size_t xeT, yT, aT, dcT, dzT, dqT, WQT, Wc2T, W1T, W1, part, sa, sb;
   size_t total;
 };
 
@@ -620,6 +620,15 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max, int m_max) {
   L.W1T = take((d + dm) * 2 * dc * 4);
   L.W1 = take(2 * dc * (d + dm) * 4);
   L.part = take(static_cast<size_t>(kColChunks) * kColGroups * std::max(d, 2 * dc) * 4);
+  // bf16 planes of the largest A and B operand of the backward's GEMMs ([rows, 3 K])
+  const size_t mk[] = {nn * d, nn * (d + dm), nn * dc, nn * 2 * dc, nn * dm, d * np, 2 * dc * np, dm * np};
+  const size_t nk[] = {dm * d, 2 * dc * (d + dm), d * dc, dc * d, (d + dm) * 2 * dc, d * dm,
+                       dc * np, (d + dm) * np, d * np};
+  size_t ma = 0, mb = 0;
+  for (size_t v : mk) ma = std::max(ma, v);
+  for (size_t v : nk) mb = std::max(mb, v);
+  L.sa = take(ma * 3 * 2);
+  L.sb = take(mb * 3 * 2);
   L.total = o;
   return L;
 }
@@ -661,10 +670,21 @@ void launch_transpose(int R, int R_pad, int C, const float* src, int64_t lds, fl
 
 template <int EPI>
 void launch_bwd_gemm(const BwdGemm& g, hipStream_t s) {
-  using C = GemmCfg<float, 64, 2>;
+  using C = BwdCfg<float>;  // same tile shape for both operand types
   const TileMap tm = make_tile_map((g.M + C::BM - 1) / C::BM, (g.N + C::BN - 1) / C::BN,
                                    static_cast<double>(g.M) * g.K, static_cast<double>(g.N) * g.K);
-  hipLaunchKernelGGL(bwd_gemm_kernel<EPI>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+  if (g.bf16)
+    hipLaunchKernelGGL((bwd_gemm_kernel<EPI, bf16_t>), dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+  else
+    hipLaunchKernelGGL((bwd_gemm_kernel<EPI, float>), dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+}
+
+void launch_split3(int R, int C, const float* src, int64_t lds, bf16_t* dst, int pattern,
+                   hipStream_t s) {
+  const int64_t total = static_cast<int64_t>(R) * C;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(split3_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, R, C, src,
+                     lds, dst, pattern);
 }
 
 BwdGemm bwd_gemm(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
@@ -679,6 +699,19 @@ BwdGemm bwd_gemm(int M, int N, int K, const float* A, int64_t lda, const float* 
   g.ldb = ldb;
   g.out = out;
   g.ldo = ldo;
+  return g;
+}
+
+// Splits A [M, K] and B [N, K] (fp32) into bf16 planes in sa / sb and returns the GEMM
+// over them (K' = 3 K); the caller launches it before the next split reuses sa / sb.
+BwdGemm split_gemm(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
+                   float* out, int64_t ldo, bf16_t* sa, bf16_t* sb, hipStream_t s) {
+  launch_split3(M, K, A, lda, sa, 0, s);
+  launch_split3(N, K, B, ldb, sb, 1, s);
+  BwdGemm g = bwd_gemm(M, N, 3 * K, nullptr, 3 * K, nullptr, 3 * K, out, ldo);
+  g.A = sa;
+  g.B = sb;
+  g.bf16 = true;
   return g;
 }
 
@@ -705,6 +738,12 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   const int np = L.npad;
   char* w = a.ws;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(w + off); };
+  // every GEMM of the backward runs on the bf16 matrix cores over its operands' planes
+  auto bwd_gemm = [&](int M, int N, int K, const float* A, int64_t lda, const float* B,
+                      int64_t ldb, float* out, int64_t ldo) {
+    return split_gemm(M, N, K, A, lda, B, ldb, out, ldo, reinterpret_cast<bf16_t*>(w + L.sa),
+                      reinterpret_cast<bf16_t*>(w + L.sb), s);
+  };
   int32_t* node_req = reinterpret_cast<int32_t*>(w + L.node_req);
   NodeInfo* info = reinterpret_cast<NodeInfo*>(w + L.info);
   float2* stats = reinterpret_cast<float2*>(w + L.stats);
@@ -854,7 +893,7 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
 // memory-build backward: workspace layout and launches
 struct MemBwdLayout {
   int npad;
-  size_t stats, xhat, xn, dxn, dkT, duT, xnT, WKT, WUT, part, total;
+  size_t stats, xhat, xn, dxn, dkT, duT, xnT, WKT, WUT, part, sa, sb, total;
 };
 
 MemBwdLayout mem_bwd_layout(const fovea_dims& D, int64_t n) {
@@ -878,6 +917,8 @@ MemBwdLayout mem_bwd_layout(const fovea_dims& D, int64_t n) {
   L.WKT = take(dv * dm * 4);
   L.WUT = take(dv * dm * 4);
   L.part = take(static_cast<size_t>(kColChunks) * kColGroups * dv * 4);
+  L.sa = take(std::max(dm * np, nn * dm) * 3 * 2);
+  L.sb = take(std::max(dv * np, dv * dm) * 3 * 2);
   L.total = o;
   return L;
 }
@@ -890,6 +931,11 @@ fovea_status run_mem_backward(fovea_ctx* c, const fovea_params* P, int n, const 
   const MemBwdLayout L = mem_bwd_layout(D, n);
   const int np = L.npad;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(w + off); };
+  auto bwd_gemm = [&](int M, int N, int K, const float* A, int64_t lda, const float* B,
+                      int64_t ldb, float* out, int64_t ldo) {
+    return split_gemm(M, N, K, A, lda, B, ldb, out, ldo, reinterpret_cast<bf16_t*>(w + L.sa),
+                      reinterpret_cast<bf16_t*>(w + L.sb), s);
+  };
   float2* stats = reinterpret_cast<float2*>(w + L.stats);
   const float* W_K = static_cast<const float*>(P->W_K);
   const float* W_U = static_cast<const float*>(P->W_U);
