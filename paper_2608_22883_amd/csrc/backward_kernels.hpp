@@ -442,10 +442,11 @@ __global__ __launch_bounds__(256) void rowsum_kernel(int rows, int len, const fl
 }
 
 // Column sums, stage 1: part[chunk][g][j] = sum over the chunk's rows i with
-// grp[i] - g0 == g of X[i][j] (* Y[i][j]); grid (ceil(cols / 256), kColChunks).
+// grp[i] - g0 == g of X[i][j] (* Y[i][j]) (* rs[i]); grid (ceil(cols / 256), kColChunks).
 __global__ __launch_bounds__(256) void colsum_part_kernel(int n, int cols, const float* __restrict__ X,
                                                           int64_t ldx, const float* __restrict__ Y,
-                                                          int64_t ldy, const int32_t* __restrict__ grp,
+                                                          int64_t ldy, const float* __restrict__ rs,
+                                                          const int32_t* __restrict__ grp,
                                                           int g0, int ng, int n_grp_total,
                                                           float* __restrict__ part) {
   const int j = blockIdx.x * 256 + threadIdx.x;
@@ -455,12 +456,23 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(int n, int cols, const
 #pragma unroll
   for (int g = 0; g < kColGroups; ++g) acc[g] = 0.f;
   if (j < cols) {
-    for (int i = i0; i < i1; ++i) {
-      float v = X[static_cast<int64_t>(i) * ldx + j];
-      if (Y != nullptr) v *= Y[static_cast<int64_t>(i) * ldy + j];
-      const int g = grp ? min(max(grp[i], 0), n_grp_total - 1) - g0 : 0;
+    if (grp == nullptr) {
+#pragma unroll 4
+      for (int i = i0; i < i1; ++i) {
+        float v = X[static_cast<int64_t>(i) * ldx + j];
+        if (Y != nullptr) v *= Y[static_cast<int64_t>(i) * ldy + j];
+        if (rs != nullptr) v *= rs[i];
+        acc[0] += v;
+      }
+    } else {
+      for (int i = i0; i < i1; ++i) {
+        float v = X[static_cast<int64_t>(i) * ldx + j];
+        if (Y != nullptr) v *= Y[static_cast<int64_t>(i) * ldy + j];
+        if (rs != nullptr) v *= rs[i];
+        const int g = min(max(grp[i], 0), n_grp_total - 1) - g0;
 #pragma unroll
-      for (int gg = 0; gg < kColGroups; ++gg) acc[gg] += gg == g ? v : 0.f;
+        for (int gg = 0; gg < kColGroups; ++gg) acc[gg] += gg == g ? v : 0.f;
+      }
     }
 #pragma unroll
     for (int g = 0; g < kColGroups; ++g)
@@ -499,6 +511,36 @@ __global__ __launch_bounds__(256) void split3_kernel(int R, int C, const float* 
     d[0] = bh;
     d[C] = pattern == 0 ? bl : bh;
     d[2 * C] = pattern == 0 ? bh : bl;
+  }
+}
+
+// The planes of src^T: dst [C, 3 R_pad] (row c holds the planes of column c of src,
+// rows R .. R_pad - 1 zero), from src [R, C] (ld lds) through 64 x 64 LDS tiles; the
+// node-axis operands of the weight-gradient GEMMs.  Grid: (ceil(C / 64), ceil(R_pad / 64)).
+__global__ __launch_bounds__(256) void transpose_split3_kernel(int R, int R_pad, int C,
+                                                               const float* __restrict__ src,
+                                                               int64_t lds, bf16_t* __restrict__ dst,
+                                                               int pattern) {
+  __shared__ float t[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    t[i][tx] = (r < R && c < C) ? src[static_cast<int64_t>(r) * lds + c] : 0.f;
+  }
+  __syncthreads();
+  const int64_t ldd = 3 * static_cast<int64_t>(R_pad);
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < C && r < R_pad) {
+      const float x = t[tx][i];
+      const float hi = bf16_round(x);
+      const bf16_t bh = f32_to_bf16_bits(hi), bl = f32_to_bf16_bits(x - hi);
+      bf16_t* d = dst + static_cast<int64_t>(c) * ldd + r;
+      d[0] = bh;
+      d[R_pad] = pattern == 0 ? bl : bh;
+      d[2 * R_pad] = pattern == 0 ? bh : bl;
+    }
   }
 }
 

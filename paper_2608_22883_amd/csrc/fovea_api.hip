@@ -571,7 +571,7 @@ struct BwdLayout {
   int npad;
   size_t node_req, info, stats, tau0, ok, dlogit, b1;
   size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe, wa, wsel;
-  size_t xeT, yT, aT, dcT, dzT, dqT, WQT, Wc2T, W1T, W1, part, sa, sb;
+  size_t WQT, Wc2T, W1T, W1, part, sa, sb;
   size_t total;
 };
 
@@ -609,12 +609,6 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max, int m_max) {
   L.dxe = take(nn * d * 4);
   L.wa = take(nn * static_cast<size_t>(m_max) * 4);
   L.wsel = take(nn * static_cast<size_t>(m_max) * 4);
-  L.xeT = take(d * np * 4);
-  L.yT = take((d + dm) * np * 4);
-  L.aT = take(2 * dc * np * 4);
-  L.dcT = take(d * np * 4);
-  L.dzT = take(2 * dc * np * 4);
-  L.dqT = take(dm * np * 4);
   L.WQT = take(d * dm * 4);
   L.Wc2T = take(dc * d * 4);
   L.W1T = take((d + dm) * 2 * dc * 4);
@@ -715,12 +709,29 @@ BwdGemm split_gemm(int M, int N, int K, const float* A, int64_t lda, const float
   return g;
 }
 
+// The weight-gradient GEMM dW = X^T Y over the node axis: X [n, M] (ld ldx) and
+// Y [n, N] (ld ldy) are transposed into bf16 planes (K = n_pad) in sa / sb.
+BwdGemm split_gemm_nodes(int n, int n_pad, int M, int N, const float* X, int64_t ldx,
+                         const float* Y, int64_t ldy, float* out, int64_t ldo, bf16_t* sa,
+                         bf16_t* sb, hipStream_t s) {
+  hipLaunchKernelGGL(transpose_split3_kernel, dim3((M + 63) / 64, (n_pad + 63) / 64), dim3(256), 0, s,
+                     n, n_pad, M, X, ldx, sa, 0);
+  hipLaunchKernelGGL(transpose_split3_kernel, dim3((N + 63) / 64, (n_pad + 63) / 64), dim3(256), 0, s,
+                     n, n_pad, N, Y, ldy, sb, 1);
+  BwdGemm g = bwd_gemm(M, N, 3 * n_pad, nullptr, 3 * n_pad, nullptr, 3 * n_pad, out, ldo);
+  g.A = sa;
+  g.B = sb;
+  g.bf16 = true;
+  return g;
+}
+
 void launch_colsum(int n, int cols, const float* X, int64_t ldx, const float* Y, int64_t ldy,
-                   const int32_t* grp, int n_groups, float* part, float* out, hipStream_t s) {
+                   const int32_t* grp, int n_groups, float* part, float* out, hipStream_t s,
+                   const float* rs = nullptr) {
   for (int g0 = 0; g0 < n_groups; g0 += kColGroups) {
     const int ng = std::min(kColGroups, n_groups - g0);
     hipLaunchKernelGGL(colsum_part_kernel, dim3((cols + 255) / 256, kColChunks), dim3(256), 0, s, n,
-                       cols, X, ldx, Y, ldy, grp, g0, ng, n_groups, part);
+                       cols, X, ldx, Y, ldy, rs, grp, g0, ng, n_groups, part);
     hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256, ng), dim3(256), 0, s, cols, g0,
                        ng, part, out);
   }
@@ -856,30 +867,24 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
                        static_cast<const float*>(a.P->q_ln_g), stats, ok, a.dh);
   }
   {
-    ProfScope ps(c, kBwdTranspose, s);
-    launch_transpose(n, np, d, F(L.xe), d, F(L.xeT), np, s);
-    launch_transpose(n, np, d + dm, F(L.y), d + dm, F(L.yT), np, s);
-    launch_transpose(n, np, 2 * dc, F(L.a), 2 * dc, F(L.aT), np, s);
-    launch_transpose(n, np, d, F(L.dc), d, F(L.dcT), np, s);
-    launch_transpose(n, np, 2 * dc, F(L.dz), 2 * dc, F(L.dzT), np, s);
-    launch_transpose(n, np, dm, F(L.dq), dm, F(L.dqT), np, s);
-  }
-  {
+    // weight gradients: GEMMs over the node axis, operands transposed into bf16 planes
     ProfScope ps(c, kBwdGemm, s);
-    launch_bwd_gemm<kEpiStore>(bwd_gemm(d, dc, np, F(L.dcT), np, F(L.aT), np, G.W_c2, dc), s);
-    BwdGemm g1 = bwd_gemm(2 * dc, d + dm, np, F(L.dzT), np, F(L.yT), np, G.W_c1, d + dm);
+    bf16_t* sa = reinterpret_cast<bf16_t*>(w + L.sa);
+    bf16_t* sb = reinterpret_cast<bf16_t*>(w + L.sb);
+    launch_bwd_gemm<kEpiStore>(split_gemm_nodes(n, np, d, dc, F(L.dc), d, F(L.a), 2 * dc, G.W_c2, dc, sa, sb, s), s);
+    BwdGemm g1 = split_gemm_nodes(n, np, 2 * dc, d + dm, F(L.dz), 2 * dc, F(L.y), d + dm, G.W_c1, d + dm, sa, sb, s);
     g1.split = dc;
     g1.out2 = G.W_g1;
     g1.ldo2 = d + dm;
     launch_bwd_gemm<kEpiRows>(g1, s);
-    launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, d, np, F(L.dqT), np, F(L.xeT), np, G.W_Q, d), s);
+    launch_bwd_gemm<kEpiStore>(split_gemm_nodes(n, np, dm, d, F(L.dq), dm, F(L.xe), d, G.W_Q, d, sa, sb, s), s);
   }
   {
     ProfScope ps(c, kBwdReduce, s);
-    launch_rowsum(d, np, F(L.dcT), np, nullptr, G.b_c2, s);
-    launch_rowsum(dc, np, F(L.dzT), np, nullptr, G.b_c1, s);
-    launch_rowsum(dc, np, F(L.dzT) + static_cast<int64_t>(dc) * np, np, nullptr, G.b_g1, s);
-    launch_rowsum(dc, np, F(L.aT) + static_cast<int64_t>(dc) * np, np, F(L.dlogit), G.w_g2, s);
+    launch_colsum(n, d, F(L.dc), d, nullptr, 0, nullptr, 1, F(L.part), G.b_c2, s);
+    launch_colsum(n, dc, F(L.dz), 2 * dc, nullptr, 0, nullptr, 1, F(L.part), G.b_c1, s);
+    launch_colsum(n, dc, F(L.dz) + dc, 2 * dc, nullptr, 0, nullptr, 1, F(L.part), G.b_g1, s);
+    launch_colsum(n, dc, F(L.a) + dc, 2 * dc, nullptr, 0, nullptr, 1, F(L.part), G.w_g2, s, F(L.dlogit));
     launch_rowsum(1, np, F(L.dlogit), np, nullptr, G.b_g2, s);
     launch_colsum(n, d, F(L.dxe), d, nullptr, 0, nullptr, 1, F(L.part), G.q_ln_b, s);
     launch_colsum(n, d, F(L.dxe), d, F(L.xhat), d, nullptr, 1, F(L.part), G.q_ln_g, s);
@@ -893,7 +898,7 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
 // memory-build backward: workspace layout and launches
 struct MemBwdLayout {
   int npad;
-  size_t stats, xhat, xn, dxn, dkT, duT, xnT, WKT, WUT, part, sa, sb, total;
+  size_t stats, xhat, xn, dxn, WKT, WUT, part, sa, sb, total;
 };
 
 MemBwdLayout mem_bwd_layout(const fovea_dims& D, int64_t n) {
@@ -911,9 +916,6 @@ MemBwdLayout mem_bwd_layout(const fovea_dims& D, int64_t n) {
   L.xhat = take(nn * dv * 4);
   L.xn = take(nn * dv * 4);
   L.dxn = take(nn * dv * 4);
-  L.dkT = take(dm * np * 4);
-  L.duT = take(dm * np * 4);
-  L.xnT = take(dv * np * 4);
   L.WKT = take(dv * dm * 4);
   L.WUT = take(dv * dm * 4);
   L.part = take(static_cast<size_t>(kColChunks) * kColGroups * dv * 4);
@@ -949,12 +951,11 @@ fovea_status run_mem_backward(fovea_ctx* c, const fovea_params* P, int n, const 
                      F(L.xhat), F(L.xn));
   launch_transpose(dm, dm, dv, W_K, dv, F(L.WKT), dm, s);
   launch_transpose(dm, dm, dv, W_U, dv, F(L.WUT), dm, s);
-  launch_transpose(n, np, dm, dk, dm, F(L.dkT), np, s);
-  launch_transpose(n, np, dm, du, dm, F(L.duT), np, s);
-  launch_transpose(n, np, dv, F(L.xn), dv, F(L.xnT), np, s);
   // weight gradients over the row axis
-  launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, dv, np, F(L.dkT), np, F(L.xnT), np, dW_K, dv), s);
-  launch_bwd_gemm<kEpiStore>(bwd_gemm(dm, dv, np, F(L.duT), np, F(L.xnT), np, dW_U, dv), s);
+  bf16_t* sa = reinterpret_cast<bf16_t*>(w + L.sa);
+  bf16_t* sb = reinterpret_cast<bf16_t*>(w + L.sb);
+  launch_bwd_gemm<kEpiStore>(split_gemm_nodes(n, np, dm, dv, dk, dm, F(L.xn), dv, dW_K, dv, sa, sb, s), s);
+  launch_bwd_gemm<kEpiStore>(split_gemm_nodes(n, np, dm, dv, du, dm, F(L.xn), dv, dW_U, dv, sa, sb, s), s);
   // dL/dLN(v) = dk W_K + du W_U
   launch_bwd_gemm<kEpiStore>(bwd_gemm(n, dv, dm, dk, dm, F(L.WKT), dm, F(L.dxn), dv), s);
   BwdGemm g2 = bwd_gemm(n, dv, dm, du, dm, F(L.WUT), dm, F(L.dxn), dv);
