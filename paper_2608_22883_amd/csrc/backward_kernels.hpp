@@ -339,7 +339,6 @@ __global__ __launch_bounds__(256) void bwd_mem_grad_kernel(int d_m, int m_max, i
   float* swa = smem_f;
   float* sws = smem_f + t_max * kMemRows;
   const int b = blockIdx.z, r0 = blockIdx.y * kMemRows;
-  const int j = blockIdx.x * 256 + threadIdx.x;
   const int64_t m0 = mem_off[b], m1 = mem_off[b + 1];
   const int t0 = node_off[b], t1 = node_off[b + 1];
   // offsets were validated per node; a request whose range is unusable is skipped here
@@ -348,36 +347,85 @@ __global__ __launch_bounds__(256) void bwd_mem_grad_kernel(int d_m, int m_max, i
   const int M = ok ? static_cast<int>(m1 - m0) : 0;
   if (r0 >= M) return;
   const int T = t1 - t0;
-  for (int e = threadIdx.x; e < T * kMemRows; e += 256) {
-    const int t = e / kMemRows, r = e % kMemRows;
-    const int64_t src = static_cast<int64_t>(t0 + t) * m_max + min(r0 + r, m_max - 1);
-    swa[e] = wa[src];
-    sws[e] = ws[src];
+  // stage the request's rows of wa / ws (eight loads in flight per thread)
+  for (int e0 = 0; e0 < T * kMemRows; e0 += 256 * 4) {
+    float va[4], vs[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = e0 + u * 256 + static_cast<int>(threadIdx.x);
+      const int t = min(e / kMemRows, T - 1), r = e % kMemRows;
+      const int64_t src = static_cast<int64_t>(t0 + t) * m_max + min(r0 + r, m_max - 1);
+      va[u] = wa[src];
+      vs[u] = ws[src];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = e0 + u * 256 + static_cast<int>(threadIdx.x);
+      if (e < T * kMemRows) {
+        swa[e] = va[u];
+        sws[e] = vs[u];
+      }
+    }
   }
   __syncthreads();
-  if (j >= d_m) return;
-  float au[kMemRows], ak[kMemRows];
+  // wave w owns memory rows r0 + 8 w .. + 7; lane l owns columns j0 .. j0 + 3
+  const int wv = threadIdx.x >> 6;
+  const int j0 = blockIdx.x * 256 + 4 * (threadIdx.x & 63);
+  if (j0 >= d_m) return;
+  float au[8][4], ak[8][4];
 #pragma unroll
-  for (int r = 0; r < kMemRows; ++r) {
-    au[r] = 0.f;
-    ak[r] = 0.f;
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      au[r][c] = 0.f;
+      ak[r][c] = 0.f;
+    }
+  // the node rows of dr and q come through a 4-deep register prefetch (a request
+  // without nodes skips the loop and writes zeros)
+  constexpr int PF = 4;
+  f32x4 drb[PF], qb[PF];
+  if (T > 0) {
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    const int tt = t0 + min(u, T - 1);
+    drb[u] = *reinterpret_cast<const f32x4*>(dr + static_cast<int64_t>(tt) * d_m + j0);
+    qb[u] = *reinterpret_cast<const f32x4*>(q + static_cast<int64_t>(tt) * d_m + j0);
   }
-#pragma unroll 4
-  for (int t = 0; t < T; ++t) {
-    const float drj = dr[static_cast<int64_t>(t0 + t) * d_m + j];
-    const float qj = q[static_cast<int64_t>(t0 + t) * d_m + j];
+  for (int tb = 0; tb < T; tb += PF) {
 #pragma unroll
-    for (int r = 0; r < kMemRows; ++r) {
-      au[r] = fmaf(swa[t * kMemRows + r], drj, au[r]);
-      ak[r] = fmaf(sws[t * kMemRows + r], qj, ak[r]);
+  for (int u = 0; u < PF; ++u) {
+    const int t = tb + u;
+    if (t >= T) break;
+    const f32x4 drv = drb[u], qv = qb[u];
+    {
+      const int tt = t0 + min(t + PF, T - 1);
+      drb[u] = *reinterpret_cast<const f32x4*>(dr + static_cast<int64_t>(tt) * d_m + j0);
+      qb[u] = *reinterpret_cast<const f32x4*>(q + static_cast<int64_t>(tt) * d_m + j0);
+    }
+    const f32x4 wa0 = *reinterpret_cast<const f32x4*>(swa + t * kMemRows + 8 * wv);
+    const f32x4 wa1 = *reinterpret_cast<const f32x4*>(swa + t * kMemRows + 8 * wv + 4);
+    const f32x4 ws0 = *reinterpret_cast<const f32x4*>(sws + t * kMemRows + 8 * wv);
+    const f32x4 ws1 = *reinterpret_cast<const f32x4*>(sws + t * kMemRows + 8 * wv + 4);
+    const float wa[8] = {wa0[0], wa0[1], wa0[2], wa0[3], wa1[0], wa1[1], wa1[2], wa1[3]};
+    const float ws[8] = {ws0[0], ws0[1], ws0[2], ws0[3], ws1[0], ws1[1], ws1[2], ws1[3]};
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        au[r][c] = fmaf(wa[r], drv[c], au[r][c]);
+        ak[r][c] = fmaf(ws[r], qv[c], ak[r][c]);
+      }
+  }
+  }
+  }
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int i = r0 + 8 * wv + r;
+    if (i < M) {
+      *reinterpret_cast<f32x4*>(dvalues + (m0 + i) * d_m + j0) = f32x4{au[r][0], au[r][1], au[r][2], au[r][3]};
+      *reinterpret_cast<f32x4*>(dkeys + (m0 + i) * d_m + j0) = f32x4{ak[r][0], ak[r][1], ak[r][2], ak[r][3]};
     }
   }
-#pragma unroll
-  for (int r = 0; r < kMemRows; ++r)
-    if (r0 + r < M) {
-      dvalues[(m0 + r0 + r) * d_m + j] = au[r];
-      dkeys[(m0 + r0 + r) * d_m + j] = ak[r];
-    }
 }
 
 // Per node: dh += LayerNorm backward of dxe g_q (xhat, rstd); rows of nodes with
@@ -498,20 +546,27 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(int cols, int g0, int
 //   A B^T = A_hi B_hi^T + A_lo B_hi^T + A_hi B_lo^T + O(2^-16)
 // is one bf16 GEMM over a tripled K with A' = [A_hi | A_lo | A_hi] (pattern 0) and
 // B' = [B_hi | B_hi | B_lo] (pattern 1).  dst [R, 3 C] row-major.
+// Grid: (ceil(C / 1024), R); thread t of block (x, r) converts columns 4 (256 x + t) ..
+// + 3 of row r (C a multiple of 4, rows 16-byte aligned).
 __global__ __launch_bounds__(256) void split3_kernel(int R, int C, const float* __restrict__ src,
                                                      int64_t lds, bf16_t* __restrict__ dst,
                                                      int pattern) {
-  const int64_t total = static_cast<int64_t>(R) * C;
-  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
-    const int r = static_cast<int>(e / C), c = static_cast<int>(e % C);
-    const float x = src[static_cast<int64_t>(r) * lds + c];
-    const float hi = bf16_round(x);
-    const bf16_t bh = f32_to_bf16_bits(hi), bl = f32_to_bf16_bits(x - hi);
-    bf16_t* d = dst + static_cast<int64_t>(r) * 3 * C + c;
-    d[0] = bh;
-    d[C] = pattern == 0 ? bl : bh;
-    d[2 * C] = pattern == 0 ? bh : bl;
+  const int r = blockIdx.y;
+  const int c = 4 * (blockIdx.x * 256 + static_cast<int>(threadIdx.x));
+  if (r >= R || c >= C) return;
+  const f32x4 x = *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(r) * lds + c);
+  uint32_t hp[2], lp[2];
+#pragma unroll
+  for (int e = 0; e < 4; e += 2) {
+    const float h0 = bf16_round(x[e]), h1 = bf16_round(x[e + 1]);
+    hp[e / 2] = pack_bf16x2(h0, h1);
+    lp[e / 2] = pack_bf16x2(x[e] - h0, x[e + 1] - h1);
   }
+  const uint2 hv = make_uint2(hp[0], hp[1]), lv = make_uint2(lp[0], lp[1]);
+  bf16_t* d = dst + static_cast<int64_t>(r) * 3 * C + c;
+  *reinterpret_cast<uint2*>(d) = hv;
+  *reinterpret_cast<uint2*>(d + C) = pattern == 0 ? lv : hv;
+  *reinterpret_cast<uint2*>(d + 2 * C) = pattern == 0 ? hv : lv;
 }
 
 // The planes of src^T: dst [C, 3 R_pad] (row c holds the planes of column c of src,

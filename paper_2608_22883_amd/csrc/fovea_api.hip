@@ -675,10 +675,8 @@ void launch_bwd_gemm(const BwdGemm& g, hipStream_t s) {
 
 void launch_split3(int R, int C, const float* src, int64_t lds, bf16_t* dst, int pattern,
                    hipStream_t s) {
-  const int64_t total = static_cast<int64_t>(R) * C;
-  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
-  hipLaunchKernelGGL(split3_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, R, C, src,
-                     lds, dst, pattern);
+  hipLaunchKernelGGL(split3_kernel, dim3((C + 1023) / 1024, R), dim3(256), 0, s, R, C, src, lds, dst,
+                     pattern);
 }
 
 BwdGemm bwd_gemm(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,

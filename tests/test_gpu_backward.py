@@ -72,6 +72,7 @@ def _compare(out, ref, tol=TOL):
     ("tiny_f32", {}, "random"),
     ("qwen_ragged", dict(B=4, T=16, M=300, M_lo=64, d=512, d_m=256, k_max=32), "random"),
     ("llava_b1", {}, "unit"),
+    ("fixed16_b32", dict(B=3, T=20), "random"),  # the paper trains with K_r fixed at 16
 ])
 def test_backward_parity(lib, name, kw, affine):
     case = make_case(_wl(name, **kw), affine=affine)
