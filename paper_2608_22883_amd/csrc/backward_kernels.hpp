@@ -569,13 +569,14 @@ __global__ __launch_bounds__(256) void split3_kernel(int R, int C, const float* 
   *reinterpret_cast<uint2*>(d + 2 * C) = pattern == 0 ? hv : lv;
 }
 
-// The planes of src^T: dst [C, 3 R_pad] (row c holds the planes of column c of src,
-// rows R .. R_pad - 1 zero), from src [R, C] (ld lds) through 64 x 64 LDS tiles; the
-// node-axis operands of the weight-gradient GEMMs.  Grid: (ceil(C / 64), ceil(R_pad / 64)).
+// The planes of src^T: row c of dst (3 W wide, planes W apart) holds column c of src
+// [R, C] (ld lds) at positions r_off .. r_off + R_pad - 1 of each plane (rows R .. R_pad - 1
+// zero), through 64 x 64 LDS tiles: the node-axis operands of the weight-gradient GEMMs
+// and the transposed weights.  Grid: (ceil(C / 64), ceil(R_pad / 64)).
 __global__ __launch_bounds__(256) void transpose_split3_kernel(int R, int R_pad, int C,
                                                                const float* __restrict__ src,
                                                                int64_t lds, bf16_t* __restrict__ dst,
-                                                               int pattern) {
+                                                               int W, int r_off, int pattern) {
   __shared__ float t[64][65];
   const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -584,17 +585,17 @@ __global__ __launch_bounds__(256) void transpose_split3_kernel(int R, int R_pad,
     t[i][tx] = (r < R && c < C) ? src[static_cast<int64_t>(r) * lds + c] : 0.f;
   }
   __syncthreads();
-  const int64_t ldd = 3 * static_cast<int64_t>(R_pad);
+  const int64_t ldd = 3 * static_cast<int64_t>(W);
   for (int i = ty; i < 64; i += 4) {
     const int c = c0 + i, r = r0 + tx;
     if (c < C && r < R_pad) {
       const float x = t[tx][i];
       const float hi = bf16_round(x);
       const bf16_t bh = f32_to_bf16_bits(hi), bl = f32_to_bf16_bits(x - hi);
-      bf16_t* d = dst + static_cast<int64_t>(c) * ldd + r;
+      bf16_t* d = dst + static_cast<int64_t>(c) * ldd + r_off + r;
       d[0] = bh;
-      d[R_pad] = pattern == 0 ? bl : bh;
-      d[2 * R_pad] = pattern == 0 ? bh : bl;
+      d[W] = pattern == 0 ? bl : bh;
+      d[2 * W] = pattern == 0 ? bh : bl;
     }
   }
 }

@@ -571,7 +571,7 @@ struct BwdLayout {
   int npad;
   size_t node_req, info, stats, tau0, ok, dlogit, b1;
   size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe, wa, wsel;
-  size_t WQT, Wc2T, W1T, W1, part, sa, sb;
+  size_t part, sa, sb;
   size_t total;
 };
 
@@ -609,10 +609,6 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max, int m_max) {
   L.dxe = take(nn * d * 4);
   L.wa = take(nn * static_cast<size_t>(m_max) * 4);
   L.wsel = take(nn * static_cast<size_t>(m_max) * 4);
-  L.WQT = take(d * dm * 4);
-  L.Wc2T = take(dc * d * 4);
-  L.W1T = take((d + dm) * 2 * dc * 4);
-  L.W1 = take(2 * dc * (d + dm) * 4);
   L.part = take(static_cast<size_t>(kColChunks) * kColGroups * std::max(d, 2 * dc) * 4);
   // bf16 planes of the largest A and B operand of the backward's GEMMs ([rows, 3 K])
   const size_t mk[] = {nn * d, nn * (d + dm), nn * dc, nn * 2 * dc, nn * dm, d * np, 2 * dc * np, dm * np};
@@ -694,6 +690,21 @@ BwdGemm bwd_gemm(int M, int N, int K, const float* A, int64_t lda, const float* 
   return g;
 }
 
+void launch_transpose_split3(int R, int R_pad, int C, const float* src, int64_t lds, bf16_t* dst,
+                             int W, int r_off, int pattern, hipStream_t s) {
+  hipLaunchKernelGGL(transpose_split3_kernel, dim3((C + 63) / 64, (R_pad + 63) / 64), dim3(256), 0, s,
+                     R, R_pad, C, src, lds, dst, W, r_off, pattern);
+}
+
+// A GEMM over bf16 planes already in sa (A', [M, 3 K]) and sb (B', [N, 3 K]).
+BwdGemm planes_gemm(int M, int N, int K, bf16_t* sa, bf16_t* sb, float* out, int64_t ldo) {
+  BwdGemm g = bwd_gemm(M, N, 3 * K, nullptr, 3 * K, nullptr, 3 * K, out, ldo);
+  g.A = sa;
+  g.B = sb;
+  g.bf16 = true;
+  return g;
+}
+
 // Splits A [M, K] and B [N, K] (fp32) into bf16 planes in sa / sb and returns the GEMM
 // over them (K' = 3 K); the caller launches it before the next split reuses sa / sb.
 BwdGemm split_gemm(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
@@ -712,10 +723,8 @@ BwdGemm split_gemm(int M, int N, int K, const float* A, int64_t lda, const float
 BwdGemm split_gemm_nodes(int n, int n_pad, int M, int N, const float* X, int64_t ldx,
                          const float* Y, int64_t ldy, float* out, int64_t ldo, bf16_t* sa,
                          bf16_t* sb, hipStream_t s) {
-  hipLaunchKernelGGL(transpose_split3_kernel, dim3((M + 63) / 64, (n_pad + 63) / 64), dim3(256), 0, s,
-                     n, n_pad, M, X, ldx, sa, 0);
-  hipLaunchKernelGGL(transpose_split3_kernel, dim3((N + 63) / 64, (n_pad + 63) / 64), dim3(256), 0, s,
-                     n, n_pad, N, Y, ldy, sb, 1);
+  launch_transpose_split3(n, n_pad, M, X, ldx, sa, n_pad, 0, 0, s);
+  launch_transpose_split3(n, n_pad, N, Y, ldy, sb, n_pad, 0, 1, s);
   BwdGemm g = bwd_gemm(M, N, 3 * n_pad, nullptr, 3 * n_pad, nullptr, 3 * n_pad, out, ldo);
   g.A = sa;
   g.B = sb;
@@ -789,16 +798,8 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
                        D.ln_eps, stats, a.depth, nd, a.node_off, a.B, a.t_max, F(L.tau0), a.mem_off,
                        a.n_mem, a.m_max, node_req, info, c->err);
   }
-  {
-    ProfScope ps(c, kBwdTranspose, s);
-    launch_transpose(dm, dm, d, W_Q, d, F(L.WQT), dm, s);
-    launch_transpose(d, d, dc, W_c2, dc, F(L.Wc2T), d, s);
-    launch_transpose(dc, dc, d + dm, W_c1, d + dm, F(L.W1T), 2 * dc, s);
-    launch_transpose(dc, dc, d + dm, W_g1, d + dm, F(L.W1T) + dc, 2 * dc, s);
-    // [W_c1; W_g1] as one operand for the layer-1 recompute: two transposes of the
-    // transposed pack give it back in [2 d_c, d + d_m]
-    launch_transpose(d + dm, d + dm, 2 * dc, F(L.W1T), 2 * dc, F(L.W1), d + dm, s);
-  }
+  bf16_t* sa = reinterpret_cast<bf16_t*>(w + L.sa);
+  bf16_t* sb = reinterpret_cast<bf16_t*>(w + L.sb);
   {
     ProfScope ps(c, kBwdPrep, s);
     hipLaunchKernelGGL(bwd_prep_kernel, dim3(n), dim3(256), 0, s, n, d, dm, a.h, stats, node_req,
@@ -818,7 +819,11 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   {
     ProfScope ps(c, kBwdGemm, s);
     // layer 1 of both nets in one GEMM (2 d_c columns); the bias is [b_c1; b_g1]
-    BwdGemm g = bwd_gemm(n, 2 * dc, d + dm, F(L.y), d + dm, F(L.W1), d + dm, F(L.z), 2 * dc);
+    // B = [W_c1; W_g1], split straight from the two weights
+    launch_split3(n, d + dm, F(L.y), d + dm, sa, 0, s);
+    launch_split3(dc, d + dm, W_c1, d + dm, sb, 1, s);
+    launch_split3(dc, d + dm, W_g1, d + dm, sb + static_cast<int64_t>(dc) * 3 * (d + dm), 1, s);
+    BwdGemm g = planes_gemm(n, 2 * dc, d + dm, sa, sb, F(L.z), 2 * dc);
     g.bias = F(L.b1);
     g.out2 = F(L.a);
     g.ldo2 = 2 * dc;
@@ -835,11 +840,18 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   }
   {
     ProfScope ps(c, kBwdGemm, s);
-    BwdGemm g = bwd_gemm(n, dc, d, F(L.dc), d, F(L.Wc2T), d, F(L.dz), 2 * dc);
+    // B = W_c2^T, transposed straight into its planes
+    launch_split3(n, d, F(L.dc), d, sa, 0, s);
+    launch_transpose_split3(d, d, dc, W_c2, dc, sb, d, 0, 1, s);
+    BwdGemm g = planes_gemm(n, dc, d, sa, sb, F(L.dz), 2 * dc);
     g.aux = F(L.z);
     g.ldaux = 2 * dc;
     launch_bwd_gemm<kEpiDsilu>(g, s);
-    BwdGemm g2 = bwd_gemm(n, d + dm, 2 * dc, F(L.dz), 2 * dc, F(L.W1T), 2 * dc, a.dh, d);
+    // B = [W_c1; W_g1]^T: the two weights transposed side by side along K
+    launch_split3(n, 2 * dc, F(L.dz), 2 * dc, sa, 0, s);
+    launch_transpose_split3(dc, dc, d + dm, W_c1, d + dm, sb, 2 * dc, 0, 1, s);
+    launch_transpose_split3(dc, dc, d + dm, W_g1, d + dm, sb, 2 * dc, dc, 1, s);
+    BwdGemm g2 = planes_gemm(n, d + dm, 2 * dc, sa, sb, a.dh, d);
     g2.split = d;
     g2.out2 = F(L.dr);
     g2.ldo2 = dm;
@@ -857,7 +869,9 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   }
   {
     ProfScope ps(c, kBwdGemm, s);
-    launch_bwd_gemm<kEpiStore>(bwd_gemm(n, d, dm, F(L.dq), dm, F(L.WQT), dm, F(L.dxe), d), s);
+    launch_split3(n, dm, F(L.dq), dm, sa, 0, s);
+    launch_transpose_split3(dm, dm, d, W_Q, d, sb, dm, 0, 1, s);
+    launch_bwd_gemm<kEpiStore>(planes_gemm(n, d, dm, sa, sb, F(L.dxe), d), s);
   }
   {
     ProfScope ps(c, kBwdLn, s);
@@ -867,8 +881,6 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   {
     // weight gradients: GEMMs over the node axis, operands transposed into bf16 planes
     ProfScope ps(c, kBwdGemm, s);
-    bf16_t* sa = reinterpret_cast<bf16_t*>(w + L.sa);
-    bf16_t* sb = reinterpret_cast<bf16_t*>(w + L.sb);
     launch_bwd_gemm<kEpiStore>(split_gemm_nodes(n, np, d, dc, F(L.dc), d, F(L.a), 2 * dc, G.W_c2, dc, sa, sb, s), s);
     BwdGemm g1 = split_gemm_nodes(n, np, 2 * dc, d + dm, F(L.dz), 2 * dc, F(L.y), d + dm, G.W_c1, d + dm, sa, sb, s);
     g1.split = dc;
