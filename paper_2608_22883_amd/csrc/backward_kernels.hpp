@@ -66,6 +66,42 @@ __device__ __forceinline__ float weighted_rows(const float* __restrict__ w, cons
   return acc;
 }
 
+// out[i] = scale * (x . rows[m0 + ix[i]]) for the entries i = wave, wave + 4, ... < K of
+// a 4-wave block (x in LDS, d_m wide): four entries at a time, each lane's loads of all
+// four issued together (512 columns per pass).
+__device__ __forceinline__ void wave_row_dots(const float* x, const int32_t* __restrict__ ix, int K,
+                                              const float* __restrict__ rows, int64_t m0, int d_m,
+                                              float scale, float* out, int wave, int lane) {
+  for (int i0 = wave; i0 < K; i0 += 16) {
+    const float* rp[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) rp[u] = rows + (m0 + ix[min(i0 + 4 * u, K - 1)]) * d_m;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int j0 = 0; j0 < d_m; j0 += 512) {
+      float v[4][8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int j = j0 + lane + 64 * t;
+          v[u][t] = j < d_m ? rp[u][j] : 0.f;
+        }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int j = j0 + lane + 64 * t;
+        const float xj = j < d_m ? x[j] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[u] = fmaf(xj, v[u][t], acc[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float sdot = wave_sum_f32(acc[u]);
+      if (lane == 0 && i0 + 4 * u < K) out[i0 + 4 * u] = sdot * scale;
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void fill_f32_kernel(int64_t count, float* __restrict__ p, float v) {
   for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < count; i += static_cast<int64_t>(gridDim.x) * 256)
     p[i] = v;
@@ -165,16 +201,8 @@ __global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m,
   #pragma unroll 8
   for (int j = tid; j < d_m; j += 256) sq[j] = q[static_cast<int64_t>(row) * d_m + j];
   __syncthreads();
-  // scores of the selected entries, one wave per entry
-  for (int i = wave; i < K; i += 4) {
-    const int64_t kr = ni.m0 + idx[static_cast<int64_t>(row) * k_max + i];
-    const float* kp = keys + kr * d_m;
-    float s = 0.f;
-    #pragma unroll 8
-    for (int j = lane; j < d_m; j += 64) s = fmaf(sq[j], kp[j], s);
-    s = wave_sum_f32(s);
-    if (lane == 0) sa[i] = s * scale;
-  }
+  // scores of the selected entries
+  wave_row_dots(sq, idx + static_cast<int64_t>(row) * k_max, K, keys, ni.m0, d_m, scale, sa, wave, lane);
   __syncthreads();
   float mx = -INFINITY;
   for (int i = tid; i < K; i += 256) mx = fmaxf(mx, sa[i]);
@@ -295,14 +323,7 @@ __global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
   #pragma unroll 8
   for (int j = tid; j < d_m; j += 256) sdr[j] = dr[static_cast<int64_t>(row) * d_m + j];
   __syncthreads();
-  for (int i = wave; i < K; i += 4) {
-    const float* up = values + (m0 + ix[i]) * d_m;
-    float s = 0.f;
-    #pragma unroll 8
-    for (int j = lane; j < d_m; j += 64) s = fmaf(sdr[j], up[j], s);
-    s = wave_sum_f32(s);
-    if (lane == 0) sds[i] = s;
-  }
+  wave_row_dots(sdr, ix, K, values, m0, d_m, 1.0f, sds, wave, lane);  // da_i = dr . u_i
   __syncthreads();
   float ad = 0.f;
   for (int i = tid; i < K; i += 256) ad = fmaf(al[i], sds[i], ad);
