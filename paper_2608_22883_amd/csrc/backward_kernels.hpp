@@ -48,20 +48,25 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// sum_{i < K} w[i] * rows[(m0 + ix[i]) * ld + j], the row loads issued eight at a time
-// so that their latencies overlap
-__device__ __forceinline__ float weighted_rows(const float* __restrict__ w, const int32_t* __restrict__ ix,
-                                               int K, const float* __restrict__ rows, int64_t m0,
-                                               int64_t ld, int j) {
-  float acc = 0.f;
+// sum_{i < K} w[i] * rows[(m0 + ix[i]) * ld + j + c] for the four columns c < 4 (16-byte loads;
+// ld and j multiples of 4), the row loads issued eight at a time so that their latencies overlap
+__device__ __forceinline__ f32x4 weighted_rows4(const float* __restrict__ w, const int32_t* __restrict__ ix,
+                                                int K, const float* __restrict__ rows, int64_t m0,
+                                                int64_t ld, int j) {
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int i0 = 0; i0 < K; i0 += 8) {
-    float v[8];
+    f32x4 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
-      v[u] = i0 + u < K ? rows[(m0 + ix[i0 + u]) * ld + j] : 0.f;
+      v[u] = i0 + u < K ? *reinterpret_cast<const f32x4*>(rows + (m0 + ix[i0 + u]) * ld + j)
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < 8; ++u)
-      if (i0 + u < K) acc = fmaf(w[i0 + u], v[u], acc);
+      if (i0 + u < K) {
+        const float wu = w[i0 + u];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = fmaf(wu, v[u][c], acc[c]);
+      }
   }
   return acc;
 }
@@ -222,9 +227,9 @@ __global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m,
   __syncthreads();
   // r = sum alpha_i u_i, columns over the threads
   const int32_t* ixr = idx + static_cast<int64_t>(row) * k_max;
-  #pragma unroll 8
-  for (int j = tid; j < d_m; j += 256)
-    y[static_cast<int64_t>(row) * (d + d_m) + d + j] = weighted_rows(sa, ixr, K, values, ni.m0, d_m, j);
+  for (int j = 4 * tid; j < d_m; j += 1024)
+    *reinterpret_cast<f32x4*>(y + static_cast<int64_t>(row) * (d + d_m) + d + j) =
+        weighted_rows4(sa, ixr, K, values, ni.m0, d_m, j);
 }
 
 // Per node: gate, h' = h + g c, RMSNorm backward, the residual split and the gate's
@@ -335,9 +340,11 @@ __global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
     wsr[ix[i]] = dsi * scale;
   }
   __syncthreads();
-  #pragma unroll 8
-  for (int j = tid; j < d_m; j += 256)
-    dq[static_cast<int64_t>(row) * d_m + j] = weighted_rows(sds, ix, K, keys, m0, d_m, j) * scale;
+  for (int j = 4 * tid; j < d_m; j += 1024) {
+    const f32x4 v = weighted_rows4(sds, ix, K, keys, m0, d_m, j);
+    *reinterpret_cast<f32x4*>(dq + static_cast<int64_t>(row) * d_m + j) =
+        f32x4{v[0] * scale, v[1] * scale, v[2] * scale, v[3] * scale};
+  }
 }
 
 // Memory gradients of one request, one tile of 32 memory rows x 256 columns per block:
