@@ -517,56 +517,129 @@ __global__ __launch_bounds__(256) void rowsum_kernel(int rows, int len, const fl
   if (lane == 0) out[r] = acc;
 }
 
-// Column sums, stage 1: part[chunk][g][j] = sum over the chunk's rows i with
-// grp[i] - g0 == g of X[i][j] (* Y[i][j]) (* rs[i]); grid (ceil(cols / 256), kColChunks).
-__global__ __launch_bounds__(256) void colsum_part_kernel(int n, int cols, const float* __restrict__ X,
-                                                          int64_t ldx, const float* __restrict__ Y,
-                                                          int64_t ldy, const float* __restrict__ rs,
-                                                          const int32_t* __restrict__ grp,
-                                                          int g0, int ng, int n_grp_total,
-                                                          float* __restrict__ part) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
+// Column sums of several row-major fp32 arrays in one launch.  A job sums over the rows
+// i < n of X (16-byte aligned, ldx and cols multiples of 4), each row scaled by rs[i] if
+// given, into up to three kinds of outputs:
+//   out_x[j]                   = sum_i X[i][j]
+//   out_xy[j]                  = sum_i X[i][j] Y[i][j]
+//   out_grp[(g0 + g) cols + j] = sum over the rows with grp[i] == g0 + g (g < ng) of X[i][j]
+// (a null output is not computed; grp values are clamped to 0 .. n_grp_total - 1).
+// Stage 1 writes per-chunk partial sums, stage 2 adds the chunks in a fixed order, so
+// every sum is deterministic.
+constexpr int kColJobs = 8;
+constexpr int kColSlots = 2 + kColGroups;
+
+struct ColJob {
+  const float* X;
+  int64_t ldx;
+  const float* Y;  // nullable (needed for out_xy)
+  int64_t ldy;
+  const float* rs;       // nullable
+  const int32_t* grp;    // nullable (needed for out_grp)
+  float* out_x;          // nullable
+  float* out_xy;         // nullable
+  float* out_grp;        // nullable
+  int g0, ng, n_grp_total;
+  int cols;
+  int64_t part_off;      // floats: this job's partials, [kColChunks][slots][cols]
+};
+
+struct ColJobs {
+  ColJob job[kColJobs];
+  int n_jobs;
+};
+
+__device__ __forceinline__ int col_job_slots(const ColJob& jb) {
+  return (jb.out_x != nullptr) + (jb.out_xy != nullptr) + (jb.out_grp != nullptr ? jb.ng : 0);
+}
+
+// Stage 1: grid (ceil(max cols / 1024), kColChunks, n_jobs); thread t of block x sums the
+// columns 4 (256 x + t) .. + 3 over the block's chunk of rows, eight rows in flight.
+__global__ __launch_bounds__(256) void colsum_multi_kernel(int n, ColJobs jobs,
+                                                           float* __restrict__ part) {
+  const ColJob& jb = jobs.job[blockIdx.z];
+  const int j = 4 * (blockIdx.x * 256 + threadIdx.x);
+  if (j >= jb.cols) return;
   const int per = (n + kColChunks - 1) / kColChunks;
   const int i0 = blockIdx.y * per, i1 = min(n, i0 + per);
-  float acc[kColGroups];
+  const bool want_x = jb.out_x != nullptr, want_xy = jb.out_xy != nullptr,
+             want_g = jb.out_grp != nullptr;
+  f32x4 ax = f32x4{0.f, 0.f, 0.f, 0.f}, axy = ax, ag[kColGroups];
 #pragma unroll
-  for (int g = 0; g < kColGroups; ++g) acc[g] = 0.f;
-  if (j < cols) {
-    if (grp == nullptr) {
-#pragma unroll 4
-      for (int i = i0; i < i1; ++i) {
-        float v = X[static_cast<int64_t>(i) * ldx + j];
-        if (Y != nullptr) v *= Y[static_cast<int64_t>(i) * ldy + j];
-        if (rs != nullptr) v *= rs[i];
-        acc[0] += v;
-      }
-    } else {
-      for (int i = i0; i < i1; ++i) {
-        float v = X[static_cast<int64_t>(i) * ldx + j];
-        if (Y != nullptr) v *= Y[static_cast<int64_t>(i) * ldy + j];
-        if (rs != nullptr) v *= rs[i];
-        const int g = min(max(grp[i], 0), n_grp_total - 1) - g0;
+  for (int g = 0; g < kColGroups; ++g) ag[g] = ax;
+  for (int ib = i0; ib < i1; ib += 8) {
+    f32x4 x[8], y[8];
 #pragma unroll
-        for (int gg = 0; gg < kColGroups; ++gg) acc[gg] += gg == g ? v : 0.f;
+    for (int u = 0; u < 8; ++u) {
+      x[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      y[u] = x[u];
+      if (ib + u < i1) {
+        x[u] = *reinterpret_cast<const f32x4*>(jb.X + static_cast<int64_t>(ib + u) * jb.ldx + j);
+        if (want_xy) y[u] = *reinterpret_cast<const f32x4*>(jb.Y + static_cast<int64_t>(ib + u) * jb.ldy + j);
       }
     }
 #pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (ib + u < i1) {
+        const float sc = jb.rs != nullptr ? jb.rs[ib + u] : 1.f;
+        f32x4 v;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          v[c] = x[u][c] * sc;
+          ax[c] += v[c];
+          axy[c] = fmaf(v[c], y[u][c], axy[c]);
+        }
+        if (want_g) {
+          const int g = min(max(jb.grp[ib + u], 0), jb.n_grp_total - 1) - jb.g0;
+#pragma unroll
+          for (int gg = 0; gg < kColGroups; ++gg) {
+            const bool hit = gg == g;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) ag[gg][c] += hit ? v[c] : 0.f;
+          }
+        }
+      }
+    }
+  }
+  const int slots = col_job_slots(jb);
+  float* pp = part + jb.part_off + static_cast<int64_t>(blockIdx.y) * slots * jb.cols + j;
+  int sl = 0;
+  if (want_x) *reinterpret_cast<f32x4*>(pp + static_cast<int64_t>(sl++) * jb.cols) = ax;
+  if (want_xy) *reinterpret_cast<f32x4*>(pp + static_cast<int64_t>(sl++) * jb.cols) = axy;
+  if (want_g) {
+#pragma unroll
     for (int g = 0; g < kColGroups; ++g)
-      if (g < ng) part[(static_cast<int64_t>(blockIdx.y) * kColGroups + g) * cols + j] = acc[g];
+      if (g < jb.ng) *reinterpret_cast<f32x4*>(pp + static_cast<int64_t>(sl + g) * jb.cols) = ag[g];
   }
 }
 
-// Column sums, stage 2: out[(g0 + g) * cols + j] = sum over chunks (fixed order).
-__global__ __launch_bounds__(256) void colsum_final_kernel(int cols, int g0, int ng,
-                                                           const float* __restrict__ part,
-                                                           float* __restrict__ out) {
+// Stage 2: grid (ceil(max cols / 256), kColSlots, n_jobs); the chunks' partials of one
+// slot added in chunk order.
+__global__ __launch_bounds__(256) void colsum_multi_final_kernel(ColJobs jobs,
+                                                                 const float* __restrict__ part) {
+  const ColJob& jb = jobs.job[blockIdx.z];
   const int j = blockIdx.x * 256 + threadIdx.x;
-  const int g = blockIdx.y;
-  if (j >= cols || g >= ng) return;
+  const int slots = col_job_slots(jb), sl = blockIdx.y;
+  if (j >= jb.cols || sl >= slots) return;
+  const float* pp = part + jb.part_off + static_cast<int64_t>(sl) * jb.cols + j;
+  const int64_t stride = static_cast<int64_t>(slots) * jb.cols;
   float acc = 0.f;
-  for (int ch = 0; ch < kColChunks; ++ch)
-    acc += part[(static_cast<int64_t>(ch) * kColGroups + g) * cols + j];
-  out[static_cast<int64_t>(g0 + g) * cols + j] = acc;
+#pragma unroll 16
+  for (int ch = 0; ch < kColChunks; ++ch) acc += pp[ch * stride];
+  int k = sl;
+  float* out;
+  if (jb.out_x != nullptr && k == 0) {
+    out = jb.out_x;
+  } else {
+    k -= jb.out_x != nullptr;
+    if (jb.out_xy != nullptr && k == 0) {
+      out = jb.out_xy;
+    } else {
+      k -= jb.out_xy != nullptr;
+      out = jb.out_grp + static_cast<int64_t>(jb.g0 + k) * jb.cols;
+    }
+  }
+  out[j] = acc;
 }
 
 // fp32 operands as bf16 planes, for GEMMs on the bf16 matrix cores with close to fp32

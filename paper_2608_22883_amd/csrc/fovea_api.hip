@@ -609,7 +609,9 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max, int m_max) {
   L.dxe = take(nn * d * 4);
   L.wa = take(nn * static_cast<size_t>(m_max) * 4);
   L.wsel = take(nn * static_cast<size_t>(m_max) * 4);
-  L.part = take(static_cast<size_t>(kColChunks) * kColGroups * std::max(d, 2 * dc) * 4);
+  // column-sum partials: b_c2, b_c1, b_g1, w_g2 and rms_w one slot each; dxe two plus
+  // one per depth
+  L.part = take(static_cast<size_t>(kColChunks) * (d * (D.n_depth + 4) + 3 * dc) * 4);
   // bf16 planes of the largest A and B operand of the backward's GEMMs ([rows, 3 K])
   const size_t mk[] = {nn * d, nn * (d + dm), nn * dc, nn * 2 * dc, nn * dm, d * np, 2 * dc * np, dm * np};
   const size_t nk[] = {dm * d, 2 * dc * (d + dm), d * dc, dc * d, (d + dm) * 2 * dc, d * dm,
@@ -732,17 +734,56 @@ BwdGemm split_gemm_nodes(int n, int n_pad, int M, int N, const float* X, int64_t
   return g;
 }
 
-void launch_colsum(int n, int cols, const float* X, int64_t ldx, const float* Y, int64_t ldy,
-                   const int32_t* grp, int n_groups, float* part, float* out, hipStream_t s,
-                   const float* rs = nullptr) {
-  for (int g0 = 0; g0 < n_groups; g0 += kColGroups) {
-    const int ng = std::min(kColGroups, n_groups - g0);
-    hipLaunchKernelGGL(colsum_part_kernel, dim3((cols + 255) / 256, kColChunks), dim3(256), 0, s, n,
-                       cols, X, ldx, Y, ldy, rs, grp, g0, ng, n_groups, part);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256, ng), dim3(256), 0, s, cols, g0,
-                       ng, part, out);
+// Column-sum jobs launched together (up to kColJobs per launch pair); every job's
+// partials get their own region of part, at increasing offsets, so part must hold
+// kColChunks x (sum over the jobs of slots x cols) floats.
+struct ColSums {
+  ColJobs js{};
+  int max_cols = 0;
+  int64_t off = 0;
+  int n;
+  float* part;
+  hipStream_t s;
+  ColSums(int n_rows, float* part_ws, hipStream_t stream) : n(n_rows), part(part_ws), s(stream) {}
+  static ColJob job(int cols, const float* X, int64_t ldx) {
+    ColJob j{};
+    j.X = X;
+    j.ldx = ldx;
+    j.cols = cols;
+    return j;
   }
-}
+  void add(ColJob jb) {
+    if (js.n_jobs == kColJobs) flush();
+    const int slots = (jb.out_x != nullptr) + (jb.out_xy != nullptr) + (jb.out_grp != nullptr ? jb.ng : 0);
+    jb.part_off = off;
+    off += static_cast<int64_t>(kColChunks) * slots * jb.cols;
+    js.job[js.n_jobs++] = jb;
+    max_cols = std::max(max_cols, jb.cols);
+  }
+  // the sums of x grouped by grp (n_groups groups), kColGroups groups per job; the first
+  // job also takes base's other outputs
+  void add_grouped(ColJob base, const int32_t* grp, int n_groups, float* out) {
+    for (int g0 = 0; g0 < n_groups; g0 += kColGroups) {
+      ColJob jb = base;
+      if (g0 > 0) jb.out_x = jb.out_xy = nullptr;
+      jb.grp = grp;
+      jb.out_grp = out;
+      jb.g0 = g0;
+      jb.ng = std::min(kColGroups, n_groups - g0);
+      jb.n_grp_total = n_groups;
+      add(jb);
+    }
+  }
+  void flush() {
+    if (js.n_jobs == 0) return;
+    hipLaunchKernelGGL(colsum_multi_kernel, dim3((max_cols + 1023) / 1024, kColChunks, js.n_jobs),
+                       dim3(256), 0, s, n, js, part);
+    hipLaunchKernelGGL(colsum_multi_final_kernel, dim3((max_cols + 255) / 256, kColSlots, js.n_jobs),
+                       dim3(256), 0, s, js, part);
+    js.n_jobs = 0;
+    max_cols = 0;
+  }
+};
 
 void launch_rowsum(int rows, int len, const float* X, int64_t ldx, const float* sc, float* out,
                    hipStream_t s) {
@@ -891,15 +932,36 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   }
   {
     ProfScope ps(c, kBwdReduce, s);
-    launch_colsum(n, d, F(L.dc), d, nullptr, 0, nullptr, 1, F(L.part), G.b_c2, s);
-    launch_colsum(n, dc, F(L.dz), 2 * dc, nullptr, 0, nullptr, 1, F(L.part), G.b_c1, s);
-    launch_colsum(n, dc, F(L.dz) + dc, 2 * dc, nullptr, 0, nullptr, 1, F(L.part), G.b_g1, s);
-    launch_colsum(n, dc, F(L.a) + dc, 2 * dc, nullptr, 0, nullptr, 1, F(L.part), G.w_g2, s, F(L.dlogit));
+    ColSums cs(n, F(L.part), s);
+    ColJob jb = ColSums::job(d, F(L.dc), d);
+    jb.out_x = G.b_c2;
+    cs.add(jb);
+    jb = ColSums::job(dc, F(L.dz), 2 * dc);
+    jb.out_x = G.b_c1;
+    cs.add(jb);
+    jb = ColSums::job(dc, F(L.dz) + dc, 2 * dc);
+    jb.out_x = G.b_g1;
+    cs.add(jb);
+    jb = ColSums::job(dc, F(L.a) + dc, 2 * dc);
+    jb.rs = F(L.dlogit);
+    jb.out_x = G.w_g2;
+    cs.add(jb);
+    if (rms_w != nullptr) {
+      jb = ColSums::job(d, a.dh_hat, d);
+      jb.Y = F(L.hn);
+      jb.ldy = d;
+      jb.out_xy = G.rms_w;
+      cs.add(jb);
+    }
+    // dxe read once for the LayerNorm bias and gain and the depth embeddings
+    jb = ColSums::job(d, F(L.dxe), d);
+    jb.Y = F(L.xhat);
+    jb.ldy = d;
+    jb.out_x = G.q_ln_b;
+    jb.out_xy = G.q_ln_g;
+    cs.add_grouped(jb, a.depth, nd, G.E_dep);
+    cs.flush();
     launch_rowsum(1, np, F(L.dlogit), np, nullptr, G.b_g2, s);
-    launch_colsum(n, d, F(L.dxe), d, nullptr, 0, nullptr, 1, F(L.part), G.q_ln_b, s);
-    launch_colsum(n, d, F(L.dxe), d, F(L.xhat), d, nullptr, 1, F(L.part), G.q_ln_g, s);
-    launch_colsum(n, d, F(L.dxe), d, nullptr, 0, a.depth, nd, F(L.part), G.E_dep, s);
-    if (rms_w != nullptr) launch_colsum(n, d, a.dh_hat, d, F(L.hn), d, nullptr, 1, F(L.part), G.rms_w, s);
   }
   FOVEA_HIP(hipGetLastError());
   return FOVEA_OK;
@@ -928,7 +990,7 @@ MemBwdLayout mem_bwd_layout(const fovea_dims& D, int64_t n) {
   L.dxn = take(nn * dv * 4);
   L.WKT = take(dv * dm * 4);
   L.WUT = take(dv * dm * 4);
-  L.part = take(static_cast<size_t>(kColChunks) * kColGroups * dv * 4);
+  L.part = take(static_cast<size_t>(kColChunks) * 2 * dv * 4);
   L.sa = take(std::max(dm * np, nn * dm) * 3 * 2);
   L.sb = take(std::max(dv * np, dv * dm) * 3 * 2);
   L.total = o;
@@ -971,8 +1033,14 @@ fovea_status run_mem_backward(fovea_ctx* c, const fovea_params* P, int n, const 
   BwdGemm g2 = bwd_gemm(n, dv, dm, du, dm, F(L.WUT), dm, F(L.dxn), dv);
   g2.split = dv;  // every column accumulates into dxn
   launch_bwd_gemm<kEpiSplit>(g2, s);
-  launch_colsum(n, dv, F(L.dxn), dv, F(L.xhat), dv, nullptr, 1, F(L.part), dg, s);
-  launch_colsum(n, dv, F(L.dxn), dv, nullptr, 0, nullptr, 1, F(L.part), db, s);
+  ColSums cs(n, F(L.part), s);
+  ColJob jb = ColSums::job(dv, F(L.dxn), dv);
+  jb.Y = F(L.xhat);
+  jb.ldy = dv;
+  jb.out_x = db;
+  jb.out_xy = dg;
+  cs.add(jb);
+  cs.flush();
   if (dV != nullptr) {
     launch_fill(dV, static_cast<int64_t>(n) * dv, s);
     hipLaunchKernelGGL(bwd_ln_kernel, dim3(n), dim3(256), 0, s, n, dv, F(L.dxn), F(L.xhat),

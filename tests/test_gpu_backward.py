@@ -82,6 +82,17 @@ def test_backward_parity(lib, name, kw, affine):
     _compare(out, ref)
 
 
+def test_backward_many_depths(lib):
+    # 27 depths: the depth-embedding sums take four column-sum jobs of at most eight depths,
+    # and the backward's column sums more jobs than one launch carries
+    case = make_case(_wl("tiny_f32", B=2, T=60, n_depth=27), affine="random")
+    case.depth = ((np.arange(case.n_nodes) * 5) % 27).astype(np.int32)
+    out, ref, st, bits, _ = _run(lib, case)
+    assert st == 0, f"data error bits {bits:#x}"
+    assert np.count_nonzero(np.abs(ref["dE_dep"]).sum(axis=1)) == 27
+    _compare(out, ref)
+
+
 def test_backward_without_rmsnorm(lib):
     case = make_case(_wl("tiny_f32", T=9, M=100), affine="random")
     out, ref, st, bits, _ = _run(lib, case, no_rms=True)
