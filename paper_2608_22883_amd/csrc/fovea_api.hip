@@ -546,10 +546,14 @@ fovea_status run_lm_topk(fovea_ctx* c, int n, const void* h, const void* W, int 
   const int d = c->dims.d;
   {
     ProfScope ps(c, kLmHead, s);
+    // row tiles: 64 for one small batch, 256 for many rows (half the operand bytes per
+    // MAC of a 128-row tile), 128 between
     if (n <= 64)
       launch_lm<T, 64>(n, static_cast<const T*>(h), d, static_cast<const T*>(W), vocab, k, cand, s);
-    else
+    else if (n < 768)
       launch_lm<T, 128>(n, static_cast<const T*>(h), d, static_cast<const T*>(W), vocab, k, cand, s);
+    else
+      launch_lm<T, 256>(n, static_cast<const T*>(h), d, static_cast<const T*>(W), vocab, k, cand, s);
   }
   {
     const int n_cand = (vocab + 127) / 128 * k;

@@ -4,7 +4,7 @@
 // experimental setup).
 //
 // Two kernels:
-//  * lm_kernel: the logit GEMM in 128 x 128 (or 64 x 128) tiles (the bf16
+//  * lm_kernel: the logit GEMM in 64, 128 or 256 x 128 tiles (the bf16
 //    direct-to-LDS mainloop of gemm.hpp) with an epilogue that keeps, for every row of
 //    the tile, its k largest logits and writes them as candidates [row][column tile][k]
 //    - the logits themselves never reach memory;
@@ -40,7 +40,7 @@
 namespace fovea {
 
 template <typename T, int BM>
-using LmCfg = GemmCfg<T, BM, 4>;
+using LmCfg = GemmCfg<T, BM, BM == 256 ? 3 : 4>;  // three 48 KB stages fit the 256-row tile
 
 constexpr int kLmMaxK = 16;
 constexpr int kLmMaxVocab = 1 << 24;
@@ -247,7 +247,11 @@ __global__ __launch_bounds__(256) void lm_kernel(LmMap tm, int n, const T* __res
                                                  const T* __restrict__ W, int vocab, int k,
                                                  uint64_t* __restrict__ cand) {
   using C = LmCfg<T, BM>;
-  __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
+  // the pipeline's stages, then the whole tile of fp32 logits
+  constexpr int kTileBytes = C::BM * C::SLD * 4;
+  constexpr int kSmem = C::SMEM_BYTES > kTileBytes ? C::SMEM_BYTES : kTileBytes;
+  static_assert(kSmem <= 160 * 1024, "LDS");
+  __shared__ __align__(16) unsigned char smem[kSmem];
   int tr, tc;
   if (!tm.map(tr, tc)) return;
   const int m0 = tr * C::BM, n0 = tc * C::BN;
@@ -261,7 +265,6 @@ __global__ __launch_bounds__(256) void lm_kernel(LmMap tm, int n, const T* __res
   float* so = reinterpret_cast<float*>(smem);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
-  static_assert(C::BM * C::SLD * 4 <= C::SMEM_BYTES, "whole-tile staging");
   constexpr int GPT = C::BM * (C::BN / 8) / C::NT;
   static_assert(GPT % 2 == 0 && C::BN / 8 == 16, "epilogue mapping");
 #pragma unroll

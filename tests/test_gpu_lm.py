@@ -87,6 +87,8 @@ def check_topk(idx, val, z, k, tol=Z_TOL):
     ("bf16", 65, 512, 4099, 1),    # arg-max, first row past one 64-row tile
     ("bf16", 7, 64, 100, 16),      # vocabulary inside one partial tile
     ("bf16", 3, 64, 16, 16),       # k = vocab: the full sort
+    ("f32", 800, 128, 1000, 6),    # 256-row tiles, the last one ragged (800 = 3 * 256 + 32)
+    ("bf16", 777, 256, 2000, 16),  # 256-row tiles, k at its limit
 ])
 def test_lm_topk_small(lib, dtype, n, d, vocab, k):
     h, W = make_lm_case(n, d, vocab, dtype, seed=n * 1000 + vocab)
