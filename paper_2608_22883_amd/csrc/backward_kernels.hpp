@@ -729,12 +729,12 @@ struct BwdGemm {
   int split;
 };
 
-template <typename T>
-using BwdCfg = GemmCfg<T, 64, 4>;
+template <typename T, int BM>
+using BwdCfg = GemmCfg<T, BM, 4>;
 
-template <int EPI, typename T>
+template <int EPI, typename T, int BM>
 __global__ __launch_bounds__(256) void bwd_gemm_kernel(TileMap tm, BwdGemm g) {
-  using C = BwdCfg<T>;
+  using C = BwdCfg<T, BM>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;

@@ -664,15 +664,28 @@ void launch_transpose(int R, int R_pad, int C, const float* src, int64_t lds, fl
                      R, R_pad, C, src, lds, dst, ldd);
 }
 
-template <int EPI>
-void launch_bwd_gemm(const BwdGemm& g, hipStream_t s) {
-  using C = BwdCfg<float>;  // same tile shape for both operand types
+template <int EPI, typename T, int BM>
+void launch_bwd_gemm_bm(const BwdGemm& g, hipStream_t s) {
+  using C = BwdCfg<T, BM>;
   const TileMap tm = make_tile_map((g.M + C::BM - 1) / C::BM, (g.N + C::BN - 1) / C::BN,
                                    static_cast<double>(g.M) * g.K, static_cast<double>(g.N) * g.K);
-  if (g.bf16)
-    hipLaunchKernelGGL((bwd_gemm_kernel<EPI, bf16_t>), dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+  hipLaunchKernelGGL((bwd_gemm_kernel<EPI, T, BM>), dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+}
+
+// 64-row tiles, or 128-row ones where they take fewer rounds of the 256 compute units
+// at about 1.5 times the time of a 64-row tile per round (bf16 operands only)
+template <int EPI>
+void launch_bwd_gemm(const BwdGemm& g, hipStream_t s) {
+  auto rounds = [&](int bm) {
+    const int64_t tiles = static_cast<int64_t>((g.M + bm - 1) / bm) * ((g.N + 127) / 128);
+    return (tiles + 255) / 256;
+  };
+  if (!g.bf16)
+    launch_bwd_gemm_bm<EPI, float, 64>(g, s);
+  else if (3 * rounds(128) < 2 * rounds(64))
+    launch_bwd_gemm_bm<EPI, bf16_t, 128>(g, s);
   else
-    hipLaunchKernelGGL((bwd_gemm_kernel<EPI, float>), dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, g);
+    launch_bwd_gemm_bm<EPI, bf16_t, 64>(g, s);
 }
 
 void launch_split3(int R, int C, const float* src, int64_t lds, bf16_t* dst, int pattern,
