@@ -353,6 +353,45 @@ __global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
 // in node order.  Grid: (ceil(d_m / 256), ceil(m_max / 32), B).
 constexpr int kMemRows = 32;
 
+// A request whose memory and node ranges are usable (the memory-gradient kernel writes
+// every row of such a request, zeros included)
+__device__ __forceinline__ bool mem_request_ok(int64_t m0, int64_t m1, int t0, int t1, int m_max,
+                                               int t_max, int n, int64_t n_mem) {
+  return 0 <= m0 && m0 <= m1 && m1 <= n_mem && m1 - m0 <= m_max && 0 <= t0 && t0 <= t1 &&
+         t1 <= n && t1 - t0 <= t_max;
+}
+
+// Zero rows of dkeys and dvalues that no usable request covers (run before
+// bwd_mem_grad_kernel, which writes all the others).  16 rows per block, 16 threads per
+// row.  The covering request is found by binary search over mem_off; where mem_off is
+// not sorted the search may miss a cover, and the zeros written are then overwritten.
+__global__ __launch_bounds__(256) void bwd_mem_gaps_kernel(int d_m, int m_max, int t_max, int B,
+                                                           const int64_t* __restrict__ mem_off,
+                                                           const int32_t* __restrict__ node_off,
+                                                           int n, int64_t n_mem,
+                                                           float* __restrict__ dkeys,
+                                                           float* __restrict__ dvalues) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 16 + (threadIdx.x >> 4);
+  if (i >= n_mem) return;
+  int lo = 0, hi = B;  // the last b < B with mem_off[b] <= i, else 0
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (mem_off[mid] <= i)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  const int64_t m0 = mem_off[lo], m1 = mem_off[lo + 1];
+  if (mem_request_ok(m0, m1, node_off[lo], node_off[lo + 1], m_max, t_max, n, n_mem) && m0 <= i &&
+      i < m1)
+    return;
+  const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 4 * (threadIdx.x & 15); j < d_m; j += 64) {
+    *reinterpret_cast<f32x4*>(dkeys + i * d_m + j) = z;
+    *reinterpret_cast<f32x4*>(dvalues + i * d_m + j) = z;
+  }
+}
+
 __global__ __launch_bounds__(256) void bwd_mem_grad_kernel(int d_m, int m_max, int t_max,
                                                            const int64_t* __restrict__ mem_off,
                                                            const int32_t* __restrict__ node_off,
@@ -370,8 +409,7 @@ __global__ __launch_bounds__(256) void bwd_mem_grad_kernel(int d_m, int m_max, i
   const int64_t m0 = mem_off[b], m1 = mem_off[b + 1];
   const int t0 = node_off[b], t1 = node_off[b + 1];
   // offsets were validated per node; a request whose range is unusable is skipped here
-  const bool ok = 0 <= m0 && m0 <= m1 && m1 <= n_mem && m1 - m0 <= m_max && 0 <= t0 &&
-                  t0 <= t1 && t1 <= n && t1 - t0 <= t_max;
+  const bool ok = mem_request_ok(m0, m1, t0, t1, m_max, t_max, n, n_mem);
   const int M = ok ? static_cast<int>(m1 - m0) : 0;
   if (r0 >= M) return;
   const int T = t1 - t0;
@@ -512,7 +550,17 @@ __global__ __launch_bounds__(256) void rowsum_kernel(int rows, int len, const fl
   if (r >= rows) return;
   const float* xr = X + static_cast<int64_t>(r) * ldx;
   float acc = 0.f;
-  for (int i = lane; i < len; i += 64) acc = fmaf(xr[i], s ? s[i] : 1.f, acc);
+  for (int i0 = lane; i0 < len; i0 += 64 * 8) {
+    float x[8], w[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + 64 * u;
+      x[u] = i < len ? xr[i] : 0.f;
+      w[u] = s != nullptr && i < len ? s[i] : 1.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc = fmaf(x[u], w[u], acc);
+  }
   acc = wave_sum_f32(acc);
   if (lane == 0) out[r] = acc;
 }
@@ -673,30 +721,51 @@ __global__ __launch_bounds__(256) void split3_kernel(int R, int C, const float* 
 // The planes of src^T: row c of dst (3 W wide, planes W apart) holds column c of src
 // [R, C] (ld lds) at positions r_off .. r_off + R_pad - 1 of each plane (rows R .. R_pad - 1
 // zero), through 64 x 64 LDS tiles: the node-axis operands of the weight-gradient GEMMs
-// and the transposed weights.  Grid: (ceil(C / 64), ceil(R_pad / 64)).
+// and the transposed weights.  Grid: (ceil(C / 64), ceil(R_pad / 64)).  Each thread
+// loads 16-byte row pieces and stores 8-byte plane pieces (four source rows): C, R_pad,
+// W, r_off and lds multiples of 4, src 16-byte and dst 8-byte aligned.
 __global__ __launch_bounds__(256) void transpose_split3_kernel(int R, int R_pad, int C,
                                                                const float* __restrict__ src,
                                                                int64_t lds, bf16_t* __restrict__ dst,
                                                                int W, int r_off, int pattern) {
   __shared__ float t[64][65];
   const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int i = ty; i < 64; i += 4) {
-    const int r = r0 + i, c = c0 + tx;
-    t[i][tx] = (r < R && c < C) ? src[static_cast<int64_t>(r) * lds + c] : 0.f;
+  const int tid = threadIdx.x;
+  // tile row (tid / 16) + 16 p, columns 4 (tid % 16) .. + 3
+  const int q = 4 * (tid & 15);
+  f32x4 v[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int r = r0 + (tid >> 4) + 16 * p, c = c0 + q;
+    v[p] = (r < R && c < C) ? *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(r) * lds + c)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
   }
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) t[(tid >> 4) + 16 * p][q + e] = v[p][e];
   __syncthreads();
+  // tile column (tid / 16) + 16 p (a row of dst), tile rows 4 (tid % 16) .. + 3
   const int64_t ldd = 3 * static_cast<int64_t>(W);
-  for (int i = ty; i < 64; i += 4) {
-    const int c = c0 + i, r = r0 + tx;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int cl = (tid >> 4) + 16 * p, c = c0 + cl, r = r0 + q;
     if (c < C && r < R_pad) {
-      const float x = t[tx][i];
-      const float hi = bf16_round(x);
-      const bf16_t bh = f32_to_bf16_bits(hi), bl = f32_to_bf16_bits(x - hi);
+      float x[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = t[q + e][cl];
+      uint32_t hp[2], lp[2];
+#pragma unroll
+      for (int e = 0; e < 4; e += 2) {
+        const float h0 = bf16_round(x[e]), h1 = bf16_round(x[e + 1]);
+        hp[e / 2] = pack_bf16x2(h0, h1);
+        lp[e / 2] = pack_bf16x2(x[e] - h0, x[e + 1] - h1);
+      }
+      const uint2 hv = make_uint2(hp[0], hp[1]), lv = make_uint2(lp[0], lp[1]);
       bf16_t* d = dst + static_cast<int64_t>(c) * ldd + r_off + r;
-      d[0] = bh;
-      d[W] = pattern == 0 ? bl : bh;
-      d[2 * W] = pattern == 0 ? bh : bl;
+      *reinterpret_cast<uint2*>(d) = hv;
+      *reinterpret_cast<uint2*>(d + W) = pattern == 0 ? lv : hv;
+      *reinterpret_cast<uint2*>(d + 2 * W) = pattern == 0 ? hv : lv;
     }
   }
 }
@@ -721,7 +790,8 @@ struct BwdGemm {
   bool bf16;
   float* out;
   int64_t ldo;
-  const float* bias;
+  const float* bias;   // nullable
+  const float* bias2;  // nullable: the bias of the columns from split on (Store, Z)
   float* out2;
   int64_t ldo2;
   const float* aux;
@@ -747,9 +817,14 @@ __global__ __launch_bounds__(256) void bwd_gemm_kernel(TileMap tm, BwdGemm g) {
       [&](int row, int col0, const float(&v)[8]) -> float {
         if (row >= g.M || col0 >= g.N) return 0.f;
         float o[8];
+        // bias of the column group: bias2 past split when given (8-column groups do not
+        // straddle split, a multiple of 8)
+        const float* bb = g.bias == nullptr ? nullptr
+                          : g.bias2 != nullptr && col0 >= g.split ? g.bias2 + (col0 - g.split)
+                                                                   : g.bias + col0;
         if (EPI == kEpiStore || EPI == kEpiZ) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = v[e] + (g.bias ? g.bias[col0 + e] : 0.f);
+          for (int e = 0; e < 8; ++e) o[e] = v[e] + (bb != nullptr ? bb[e] : 0.f);
           store8(g.out + static_cast<int64_t>(row) * g.ldo + col0, o);
           if (EPI == kEpiZ) {
 #pragma unroll

@@ -573,7 +573,7 @@ fovea_status run_lm_topk(fovea_ctx* c, int n, const void* h, const void* W, int 
 
 struct BwdLayout {
   int npad;
-  size_t node_req, info, stats, tau0, ok, dlogit, b1;
+  size_t node_req, info, stats, tau0, ok, dlogit;
   size_t xhat, xe, y, q, alpha, z, a, c, hn, dc, dz, dr, dq, dxe, wa, wsel;
   size_t part, sa, sb;
   size_t total;
@@ -596,7 +596,6 @@ BwdLayout bwd_layout(const fovea_dims& D, int B, int n, int k_max, int m_max) {
   L.tau0 = take(static_cast<size_t>(B) * 4);
   L.ok = take(nn * 4);
   L.dlogit = take(np * 4);
-  L.b1 = take(2 * dc * 4);
   L.xhat = take(nn * d * 4);
   L.xe = take(nn * d * 4);
   L.y = take(nn * (d + dm) * 4);
@@ -845,11 +844,11 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
     ProfScope ps(c, kBwdFill, s);
     launch_fill(F(L.tau0), a.B, s);
     launch_fill(F(L.dlogit), np, s);
-    launch_fill(a.dkeys, a.n_mem * dm, s);
-    launch_fill(a.dvalues, a.n_mem * dm, s);
+    if (a.n_mem > 0)
+      hipLaunchKernelGGL(bwd_mem_gaps_kernel, dim3(static_cast<unsigned>((a.n_mem + 15) / 16)), dim3(256), 0,
+                         s, dm, a.m_max, a.t_max, a.B, a.mem_off, a.node_off, n, a.n_mem, a.dkeys,
+                         a.dvalues);
   }
-  FOVEA_HIP(hipMemcpyAsync(F(L.b1), a.P->b_c1, dc * 4, hipMemcpyDeviceToDevice, s));
-  FOVEA_HIP(hipMemcpyAsync(F(L.b1) + dc, a.P->b_g1, dc * 4, hipMemcpyDeviceToDevice, s));
   {
     ProfScope ps(c, kBwdStats, s);
     hipLaunchKernelGGL(row_stats_kernel<float>, dim3((n + 3) / 4), dim3(256), 0, s, n, a.h, d,
@@ -882,7 +881,9 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
     launch_split3(dc, d + dm, W_c1, d + dm, sb, 1, s);
     launch_split3(dc, d + dm, W_g1, d + dm, sb + static_cast<int64_t>(dc) * 3 * (d + dm), 1, s);
     BwdGemm g = planes_gemm(n, 2 * dc, d + dm, sa, sb, F(L.z), 2 * dc);
-    g.bias = F(L.b1);
+    g.bias = static_cast<const float*>(a.P->b_c1);
+    g.bias2 = static_cast<const float*>(a.P->b_g1);
+    g.split = dc;
     g.out2 = F(L.a);
     g.ldo2 = 2 * dc;
     launch_bwd_gemm<kEpiZ>(g, s);
@@ -1365,7 +1366,8 @@ fovea_status fovea_retrieve_fuse_backward(
   const void* wreq[] = {p->q_ln_g, p->q_ln_b, p->E_dep, p->W_Q, p->W_c1, p->b_c1,
                         p->W_c2,   p->b_c2,   p->W_g1,  p->b_g1, p->w_g2};
   for (const void* r : wreq)
-    if (r == nullptr) return FOVEA_ERR_INVALID_ARG;
+    if (r == nullptr || !aligned16(r)) return FOVEA_ERR_INVALID_ARG;
+  if (p->rms_w != nullptr && !aligned16(p->rms_w)) return FOVEA_ERR_INVALID_ARG;
   float* greq[] = {g->W_Q, g->q_ln_g, g->q_ln_b, g->E_dep, g->W_c1, g->b_c1, g->W_c2,
                    g->b_c2, g->W_g1, g->b_g1, g->w_g2, g->b_g2};
   for (float* r : greq)

@@ -2,6 +2,8 @@
 retrieve_fuse_backward, through the C ABI.  The selection both sides hold fixed is the
 oracle forward's own (an input of the backward)."""
 
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -90,6 +92,29 @@ def test_backward_many_depths(lib):
     out, ref, st, bits, _ = _run(lib, case)
     assert st == 0, f"data error bits {bits:#x}"
     assert np.count_nonzero(np.abs(ref["dE_dep"]).sum(axis=1)) == 27
+    _compare(out, ref)
+
+
+def test_backward_memory_rows_outside_every_request(lib):
+    # 5 memory rows before the first request and 3 after the last: their gradients are zero
+    case = make_case(_wl("tiny_f32", B=2, T=9, M=100), affine="random")
+    rng = np.random.default_rng(5)
+
+    def pad(x):
+        lead = rng.standard_normal((5, x.shape[1])).astype(np.float32).astype(np.float64)
+        tail = rng.standard_normal((3, x.shape[1])).astype(np.float32).astype(np.float64)
+        return np.concatenate([lead, x, tail])
+
+    case = dataclasses.replace(case, keys=pad(case.keys), values=pad(case.values),
+                               mem_off=case.mem_off + 5)
+    # NaN-filled blocks of the outputs' size, freed so that the outputs likely reuse them
+    junk = [torch.full((case.keys.shape[0], case.workload.d_m), float("nan"), device="cuda")
+            for _ in range(4)]
+    del junk
+    out, ref, st, bits, _ = _run(lib, case)
+    assert st == 0, f"data error bits {bits:#x}"
+    for k in ("dkeys", "dvalues"):
+        assert np.all(out[k][:5] == 0) and np.all(out[k][-3:] == 0), k
     _compare(out, ref)
 
 
