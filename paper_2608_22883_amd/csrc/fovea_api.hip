@@ -72,6 +72,11 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 // Byte offsets of the retrieve_fuse workspace regions.
+// k-sliced scores (score_parts): batches of at most kScoreSplitNodes nodes may split
+// the score GEMM's d_m into up to kScoreMaxParts slices
+constexpr int kScoreSplitNodes = 256;
+constexpr int kScoreMaxParts = 4;
+
 struct WsLayout {
   size_t node_req, info, stats, q, P, S, rT, a_c, gate_part, rms_part, splitk, total;
 };
@@ -100,7 +105,9 @@ WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
   L.stats = o; o = align_up(o + n * 8);
   L.q = o; o = align_up(o + n * dm.d_m * (dm.dtype == FOVEA_BF16 ? 2 * kQSplitBf16 : 4));
   L.P = o; o = align_up(o + n * 2 * dm.d_c * 4);
-  L.S = o; o = align_up(o + n * m_max * 4);
+  // scores; small bf16 batches may hold k-sliced partial scores (score_parts)
+  const int64_t s_arrays = dm.dtype == FOVEA_BF16 && n <= kScoreSplitNodes ? kScoreMaxParts : 1;
+  L.S = o; o = align_up(o + s_arrays * n * m_max * 4);
   L.rT = o; o = align_up(o + n * dm.d_m * es);
   L.a_c = o; o = align_up(o + n * dm.d_c * es);
   L.gate_part = o; o = align_up(o + n * n_parts(2 * dm.d_c) * 4);
@@ -302,7 +309,7 @@ int score_keys_per_block(int B, int m_max) {
 }
 
 typedef void (*ScoreKernel)(int, const int64_t*, int64_t, int, const int32_t*, int, int,
-                            const bf16_t*, int, const bf16_t*, float, float*);
+                            const bf16_t*, int, const bf16_t*, float, float*, int);
 
 template <int NKC>
 ScoreKernel score_kernel_kb(int kb) {
@@ -329,6 +336,25 @@ ScoreKernel score_kernel_for(int nkc, int kb) {
   }
 }
 
+// k slices of the bf16 score GEMM.  A small batch's score grid leaves most compute units
+// idle while each block streams all of its nodes' q (256 d_m bytes), so d_m is cut into
+// 2 or 4 slices (each an instantiated chunk count) whose partial scores the selection
+// adds in order.  Only batches of at most kScoreSplitNodes nodes, for which the
+// workspace holds kScoreMaxParts score arrays.
+
+int score_parts(const fovea_dims& D, int B, int n, int m_max, int t_max) {
+  if (D.dtype != FOVEA_BF16 || n > kScoreSplitNodes || m_max == 0 || t_max == 0) return 1;
+  const int kb = score_keys_per_block(B, m_max) / 16;
+  const int64_t blocks = static_cast<int64_t>(B) * ((m_max + 16 * kb - 1) / (16 * kb)) *
+                         ((t_max + 63) / 64);
+  const int nkc = D.d_m / score_cfg::KC;
+  int best = 1;
+  for (int p = 2; p <= kScoreMaxParts; p *= 2)
+    if (nkc % p == 0 && blocks * p <= 256 && score_kernel_for(nkc / p, kb) != score_bf16_any_kernel)
+      best = p;
+  return best;
+}
+
 template <typename T>
 fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   const fovea_dims& D = c->dims;
@@ -341,6 +367,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   T* q = reinterpret_cast<T*>(a.ws + L.q);
   float* P = reinterpret_cast<float*>(a.ws + L.P);
   float* S = reinterpret_cast<float*>(a.ws + L.S);
+  const int s_parts = score_parts(D, a.B, a.n, a.m_max, a.t_max);
   T* rT = reinterpret_cast<T*>(a.ws + L.rT);
   T* a_c = reinterpret_cast<T*>(a.ws + L.a_c);
   float* gate_part = reinterpret_cast<float*>(a.ws + L.gate_part);
@@ -388,13 +415,13 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     if constexpr (std::is_same<T, bf16_t>::value) {
       const int kb = score_keys_per_block(a.B, a.m_max) / 16;
       const int tiles = (a.m_max + 16 * kb - 1) / (16 * kb);
-      auto kern = score_kernel_for(D.d_m / score_cfg::KC, kb);
+      auto kern = score_kernel_for(D.d_m / score_cfg::KC / s_parts, kb);
       const int nch = (a.t_max + 63) / 64;
       const int grid = xcd_grid(kern == score_bf16_any_kernel ? a.B * ((a.m_max + 63) / 64)
-                                                              : a.B * tiles * nch);
+                                                              : a.B * tiles * nch * s_parts);
       hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, a.B, a.mem_off, a.n_mem, a.m_max,
                          a.node_off, a.n, a.t_max, static_cast<const bf16_t*>(a.keys), D.d_m,
-                         reinterpret_cast<const bf16_t*>(q), scale, S);
+                         reinterpret_cast<const bf16_t*>(q), scale, S, s_parts);
     } else {
       const int tiles = (a.m_max + 63) / 64;
       hipLaunchKernelGGL(score_f32_kernel, dim3(xcd_grid(a.B * tiles)), dim3(256), 0, s, a.B,
@@ -415,6 +442,8 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   sa.values = static_cast<const T*>(a.values);
   sa.d_m = D.d_m;
   sa.S = S;
+  sa.s_parts = s_parts;
+  sa.s_stride = static_cast<int64_t>(a.n) * a.m_max;
   sa.k_min = a.k_min;
   sa.k_max = a.k_max;
   sa.rT = rT;

@@ -327,17 +327,21 @@ template <int NKC, int KB>
 __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf16_kernel(
     int B, const int64_t* __restrict__ mem_off, int64_t n_mem, int m_max,
     const int32_t* __restrict__ node_off, int n_nodes, int t_max, const bf16_t* __restrict__ keys,
-    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S) {
+    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S, int parts) {
   using namespace score_cfg;
   using TL = Tile<KB>;
   __shared__ __align__(16) bf16_t ks[2][TL::ROWS][LDK];
   const int tiles = (m_max + TL::KT - 1) / TL::KT;
   const int nch = (t_max + 63) / 64;  // 64-node chunks; a block takes one
-  const int item = xcd_item(B * tiles * nch);
-  if (item < 0) return;
+  // parts > 1: the block contracts k slice `part` (NKC chunks) of d_m = parts NKC KC and
+  // writes partial scores to S + part n_nodes m_max (the selection adds them in order)
+  const int item0 = xcd_item(B * tiles * nch * parts);
+  if (item0 < 0) return;
+  const int part = item0 % parts, item = item0 / parts;
   const int b = item / (tiles * nch);
   const int tile = (item / nch) % tiles;
   const int cn = (item % nch) * 64;
+  const int kofs0 = part * NKC * KC;
   const Extent e = request_extent(b, mem_off, n_mem, m_max, node_off, n_nodes, t_max);
   if (!e.nodes_ok || !e.mem_ok) return;  // the select kernel reports and fills NaN
   const int M = static_cast<int>(e.m1 - e.m0);
@@ -354,7 +358,7 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
   for (int u = 0; u < TL::KCH; ++u) {
     const int qi = tid + 256 * u;               // 16-byte chunk of the [rows][64] tile
     const int row = qi >> 3, kofs = (qi & 7) * 8;
-    kg[u] = keys + (e.m0 + min(i0 + row, M - 1)) * d_m + kofs;
+    kg[u] = keys + (e.m0 + min(i0 + row, M - 1)) * d_m + kofs0 + kofs;
     kd0[u] = reinterpret_cast<u32x4*>(&ks[0][row][kofs]);
     kd1[u] = reinterpret_cast<u32x4*>(&ks[1][row][kofs]);
   }
@@ -363,7 +367,7 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
 
   {
     const int qrow = e.t0 + min(cn + 16 * w + (lane & 15), Tn - 1);
-    const bf16_t* qg = q + static_cast<int64_t>(qrow) * d_m + 16 * g;
+    const bf16_t* qg = q + static_cast<int64_t>(qrow) * d_m + kofs0 + 16 * g;
     u32x4 kr[DK][TL::KCH];
     u32x4 qr[DK][NS][2];
     f32x4 acc[KB];
@@ -433,6 +437,7 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
       __syncthreads();
     }
     if (cn + 16 * w < Tn) {
+      float* Sp = S + static_cast<int64_t>(part) * n_nodes * m_max;
 #pragma unroll
       for (int kblk = 0; kblk < KB; ++kblk) {
         const int key = i0 + kblk * 16 + (lane & 15);
@@ -440,7 +445,7 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int r = cn + 16 * w + 4 * g + v;
-          if (r < Tn) S[static_cast<int64_t>(e.t0 + r) * m_max + key] = acc[kblk][v] * scale;
+          if (r < Tn) Sp[static_cast<int64_t>(e.t0 + r) * m_max + key] = acc[kblk][v] * scale;
         }
       }
     }
@@ -452,7 +457,7 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
 __global__ __launch_bounds__(256) void score_bf16_any_kernel(
     int B, const int64_t* __restrict__ mem_off, int64_t n_mem, int m_max,
     const int32_t* __restrict__ node_off, int n_nodes, int t_max, const bf16_t* __restrict__ keys,
-    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S) {
+    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S, int /*parts: 1*/) {
   using namespace score_cfg;
   constexpr int KT = 64;
   __shared__ __align__(16) bf16_t ks[KT][LDK];
@@ -605,6 +610,8 @@ struct SelectArgs {
   const T* values;
   int d_m;
   const float* S;
+  int s_parts;        // partial score arrays to add (in order), s_stride floats apart
+  int64_t s_stride;
   int k_min, k_max;
   T* rT;
   float* r_out;
@@ -740,7 +747,9 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   uint32_t kmax = 0;
   for (int i = tid; i < M; i += NT) {
     const bool v = a.valid == nullptr || a.valid[m0 + i] != 0;
-    const uint32_t k = v ? order_key(srow[i]) : 0u;
+    float sc = srow[i];
+    for (int p = 1; p < a.s_parts; ++p) sc += srow[p * a.s_stride + i];
+    const uint32_t k = v ? order_key(sc) : 0u;
     skey[i] = k;
     cnt += v ? 1 : 0;
     kmax = max(kmax, k);
@@ -1028,6 +1037,13 @@ __device__ __forceinline__ NodeKeys load_node_keys(const SelectArgs<T>& a, int n
   float sv[NPL];
 #pragma unroll
   for (int j = 0; j < NPL; ++j) sv[j] = a.m_max > 0 ? srow[min(lane + 64 * j, a.m_max - 1)] : 0.f;
+  for (int p = 1; p < a.s_parts && a.m_max > 0; ++p) {
+    float pv[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) pv[j] = srow[p * a.s_stride + min(lane + 64 * j, a.m_max - 1)];
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) sv[j] += pv[j];
+  }
   const NodeInfo inf = a.info[n];
   NodeKeys r;
   r.ok = inf.M >= 0;
