@@ -75,7 +75,6 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 // k-sliced scores (score_parts): batches of at most kScoreSplitNodes nodes may split
 // the score GEMM's d_m into up to kScoreMaxParts slices
 constexpr int kScoreSplitNodes = 256;
-constexpr int kScoreMaxParts = 4;
 
 struct WsLayout {
   size_t node_req, info, stats, q, P, S, rT, a_c, gate_part, rms_part, splitk, total;

@@ -598,6 +598,8 @@ __global__ __launch_bounds__(256) void score_f32_kernel(int B, const int64_t* __
 //   cumulative-mass rule; renormalised weights; weighted gather of value rows.
 // ---------------------------------------------------------------------------------
 
+constexpr int kScoreMaxParts = 4;  // k slices of the score GEMM (partial score arrays)
+
 template <typename T>
 struct SelectArgs {
   const int64_t* mem_off;
@@ -747,8 +749,12 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   uint32_t kmax = 0;
   for (int i = tid; i < M; i += NT) {
     const bool v = a.valid == nullptr || a.valid[m0 + i] != 0;
-    float sc = srow[i];
-    for (int p = 1; p < a.s_parts; ++p) sc += srow[p * a.s_stride + i];
+    float sc = srow[i], ps[kScoreMaxParts - 1];
+#pragma unroll
+    for (int p = 1; p < kScoreMaxParts; ++p) ps[p - 1] = p < a.s_parts ? srow[p * a.s_stride + i] : 0.f;
+#pragma unroll
+    for (int p = 1; p < kScoreMaxParts; ++p)
+      if (p < a.s_parts) sc += ps[p - 1];
     const uint32_t k = v ? order_key(sc) : 0u;
     skey[i] = k;
     cnt += v ? 1 : 0;
@@ -1037,13 +1043,18 @@ __device__ __forceinline__ NodeKeys load_node_keys(const SelectArgs<T>& a, int n
   float sv[NPL];
 #pragma unroll
   for (int j = 0; j < NPL; ++j) sv[j] = a.m_max > 0 ? srow[min(lane + 64 * j, a.m_max - 1)] : 0.f;
-  for (int p = 1; p < a.s_parts && a.m_max > 0; ++p) {
-    float pv[NPL];
+  // partial scores of the other k slices: every load issued before the first add
+  float pv[kScoreMaxParts - 1][NPL];
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) pv[j] = srow[p * a.s_stride + min(lane + 64 * j, a.m_max - 1)];
+  for (int p = 1; p < kScoreMaxParts; ++p)
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) sv[j] += pv[j];
-  }
+    for (int j = 0; j < NPL; ++j)
+      pv[p - 1][j] = p < a.s_parts && a.m_max > 0 ? srow[p * a.s_stride + min(lane + 64 * j, a.m_max - 1)] : 0.f;
+#pragma unroll
+  for (int p = 1; p < kScoreMaxParts; ++p)
+#pragma unroll
+    for (int j = 0; j < NPL; ++j)
+      if (p < a.s_parts) sv[j] += pv[p - 1][j];
   const NodeInfo inf = a.info[n];
   NodeKeys r;
   r.ok = inf.M >= 0;
