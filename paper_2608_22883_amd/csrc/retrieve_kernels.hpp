@@ -698,6 +698,31 @@ __device__ __forceinline__ RadixPick radix_pick(int* hist, int krem, RadixPick* 
   return *out;
 }
 
+// Sorts the C distinct keys of list descending in place: the rank of a key is the number
+// of keys above it, counted in one broadcast pass over the list (thread tid ranks the
+// keys at tid + NT q, q < Q).
+template <int Q, int NT>
+__device__ __forceinline__ void rank_sort_desc(unsigned long long* list, int C, int tid) {
+  unsigned long long mine[Q];
+  int rk[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int t = tid + NT * q;
+    mine[q] = t < C ? list[t] : 0ull;
+    rk[q] = 0;
+  }
+  for (int j = 0; j < C; ++j) {
+    const unsigned long long y = list[j];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) rk[q] += y > mine[q] ? 1 : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+    if (tid + NT * q < C) list[rk[q]] = mine[q];
+  __syncthreads();
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   constexpr int NT = 256;
@@ -838,28 +863,14 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
     __syncthreads();
     // s_count equals C by construction; never let a short count expose stale slots
     const int C_ok = min(C, s_count);
-    int P = 1;
-    while (P < C) P <<= 1;
-    for (int i = C_ok + tid; i < C; i += NT) cand[i] = 0ull;
-    for (int i = C + tid; i < P; i += NT) cand[i] = 0ull;
+    // (distinct values below every real key, which has a nonzero high word)
+    for (int i = C_ok + tid; i < C; i += NT) cand[i] = static_cast<unsigned long long>(C - i);
     __syncthreads();
-    // bitonic sort, descending
-    for (int kk = 2; kk <= P; kk <<= 1) {
-      for (int j = kk >> 1; j > 0; j >>= 1) {
-        for (int i = tid; i < P; i += NT) {
-          const int ixj = i ^ j;
-          if (ixj > i) {
-            const unsigned long long x = cand[i], y = cand[ixj];
-            const bool desc = (i & kk) == 0;
-            if (desc ? (x < y) : (x > y)) {
-              cand[i] = y;
-              cand[ixj] = x;
-            }
-          }
-        }
-        __syncthreads();
-      }
-    }
+    // descending order by counting (the keys are distinct: each holds its entry index)
+    if (C <= NT)
+      rank_sort_desc<1, NT>(cand, C, tid);
+    else
+      rank_sort_desc<kMaxKmax / NT, NT>(cand, C, tid);
     // prefix sums of exp(s - max) in rank order, four consecutive ranks per thread
     double e4[4];
     double loc = 0.0;
@@ -893,11 +904,18 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
     }
     if (tid == 0) s_first = INT_MAX;
     __syncthreads();
+    // the first rank whose prefix reaches tau Z: the prefixes only grow with the rank, so
+    // a wave's first qualifying rank sits in its lowest qualifying lane (one atomic per wave)
     const double tau = static_cast<double>(a.tau[b]);
+    {
+      int first = INT_MAX;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = 4 * tid + j;
-      if (t < C && pre[t] / Z >= tau) atomicMin(&s_first, t);
+      for (int j = 3; j >= 0; --j) {
+        const int t = 4 * tid + j;
+        if (t < C && pre[t] / Z >= tau) first = t;
+      }
+      const unsigned long long hit = __ballot(first != INT_MAX);
+      if (hit != 0ull && (tid & 63) == __ffsll(static_cast<long long>(hit)) - 1) atomicMin(&s_first, first);
     }
     __syncthreads();
     const int K_raw = s_first != INT_MAX ? s_first + 1 : (C == nV ? nV : a.k_max + 1);
@@ -933,22 +951,33 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
       float acc[VEC];
 #pragma unroll
       for (int x = 0; x < VEC; ++x) acc[x] = 0.f;
-      for (int q0 = 0; q0 < mine; q0 += GR) {
-        const int nr = min(GR, mine - q0);
-        u32x4 raw[GR];
+      // batches of 2 GR rows while that many remain, then of up to GR
+      auto batch = [&](auto G_, int q0, int nr) {
+        constexpr int G = decltype(G_)::value;
+        u32x4 raw[G];
 #pragma unroll
-        for (int r = 0; r < GR; ++r) {
+        for (int r = 0; r < G; ++r) {
           const int t = w + 4 * (q0 + min(r, nr - 1));
           raw[r] = *reinterpret_cast<const u32x4*>(a.values + (m0 + sidx[t]) * a.d_m + c * VEC);
         }
 #pragma unroll
-        for (int r = 0; r < GR; ++r) {
+        for (int r = 0; r < G; ++r) {
           if (r < nr) {
             const float wt = alpha[w + 4 * (q0 + r)];
             const T* v = reinterpret_cast<const T*>(&raw[r]);
 #pragma unroll
             for (int x = 0; x < VEC; ++x) acc[x] = fmaf(wt, Elem<T>::to_f32(v[x]), acc[x]);
           }
+        }
+      };
+      for (int q0 = 0; q0 < mine;) {
+        if (mine - q0 >= 2 * GR) {
+          batch(std::integral_constant<int, 2 * GR>(), q0, 2 * GR);
+          q0 += 2 * GR;
+        } else {
+          const int nr = min(GR, mine - q0);
+          batch(std::integral_constant<int, GR>(), q0, nr);
+          q0 += nr;
         }
       }
       if (w > 0)
