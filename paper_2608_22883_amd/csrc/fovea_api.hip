@@ -455,7 +455,10 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     ProfScope ps(c, kSelect, s);
     const int VEC = D.dtype == FOVEA_BF16 ? 8 : 4;
     const int nch = (D.d_m / VEC + 63) / 64;  // 16-byte chunks per lane per value row
-    const bool wave_path = a.k_max <= kWaveSelKmax && a.m_max <= 64 * 64 && nch <= 4;
+    // one wave selects a node of at most 1024 entries (16 keys per lane); larger memories
+    // go to the block-wide kernel, whose radix threshold and counting rank use all four
+    // waves (ragged Qwen workload, memories of up to 4096: 98.6 -> 41.4 us)
+    const bool wave_path = a.k_max <= kWaveSelKmax && a.m_max <= 1024 && nch <= 4;
     if (wave_path) {
       // one node per block when the pairs would leave compute units idle: the gather of a
       // node then runs on four waves instead of two
@@ -477,11 +480,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
       else if (npl <= 6) { FOVEA_SEL(6); }
       else if (npl <= 9) { FOVEA_SEL(9); }
       else if (npl <= 12) { FOVEA_SEL(12); }
-      else if (npl <= 16) { FOVEA_SEL(16); }
-      else if (npl <= 24) { FOVEA_SEL(24); }
-      else if (npl <= 32) { FOVEA_SEL(32); }
-      else if (npl <= 48) { FOVEA_SEL(48); }
-      else { FOVEA_SEL(64); }
+      else { FOVEA_SEL(16); }
 #undef FOVEA_SEL
 #undef FOVEA_SEL_C
     } else {

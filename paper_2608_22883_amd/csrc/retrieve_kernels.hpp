@@ -594,7 +594,7 @@ __global__ __launch_bounds__(256) void score_f32_kernel(int B, const int64_t* __
 // Per-node selection and gather, one 256-thread block per node:
 //   max and Z over the valid scores; exact top-k_max by (score desc, index asc) with an
 //   MSB-first radix select on the order-preserving score key (plus, for ties, on the
-//   inverted index); bitonic sort of the candidates; prefix masses in fp64; K from the
+//   inverted index); candidates ranked by counting; prefix masses in fp64; K from the
 //   cumulative-mass rule; renormalised weights; weighted gather of value rows.
 // ---------------------------------------------------------------------------------
 
