@@ -308,7 +308,7 @@ int score_keys_per_block(int B, int m_max) {
 }
 
 typedef void (*ScoreKernel)(int, const int64_t*, int64_t, int, const int32_t*, int, int,
-                            const bf16_t*, int, const bf16_t*, float, float*, int);
+                            const bf16_t*, int, const bf16_t*, float, float*, int, int);
 
 template <int NKC>
 ScoreKernel score_kernel_kb(int kb) {
@@ -416,11 +416,13 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
       const int tiles = (a.m_max + 16 * kb - 1) / (16 * kb);
       auto kern = score_kernel_for(D.d_m / score_cfg::KC / s_parts, kb);
       const int nch = (a.t_max + 63) / 64;
+      // ragged memories (their total well below B m_max): spread the tiles over the XCDs
+      const int spread = a.n_mem * 4 < static_cast<int64_t>(a.B) * a.m_max * 3 ? 1 : 0;
       const int grid = xcd_grid(kern == score_bf16_any_kernel ? a.B * ((a.m_max + 63) / 64)
                                                               : a.B * tiles * nch * s_parts);
       hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, a.B, a.mem_off, a.n_mem, a.m_max,
                          a.node_off, a.n, a.t_max, static_cast<const bf16_t*>(a.keys), D.d_m,
-                         reinterpret_cast<const bf16_t*>(q), scale, S, s_parts);
+                         reinterpret_cast<const bf16_t*>(q), scale, S, s_parts, spread);
     } else {
       const int tiles = (a.m_max + 63) / 64;
       hipLaunchKernelGGL(score_f32_kernel, dim3(xcd_grid(a.B * tiles)), dim3(256), 0, s, a.B,

@@ -327,7 +327,8 @@ template <int NKC, int KB>
 __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf16_kernel(
     int B, const int64_t* __restrict__ mem_off, int64_t n_mem, int m_max,
     const int32_t* __restrict__ node_off, int n_nodes, int t_max, const bf16_t* __restrict__ keys,
-    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S, int parts) {
+    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S, int parts,
+    int spread) {
   using namespace score_cfg;
   using TL = Tile<KB>;
   __shared__ __align__(16) bf16_t ks[2][TL::ROWS][LDK];
@@ -335,7 +336,11 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
   const int nch = (t_max + 63) / 64;  // 64-node chunks; a block takes one
   // parts > 1: the block contracts k slice `part` (NKC chunks) of d_m = parts NKC KC and
   // writes partial scores to S + part n_nodes m_max (the selection adds them in order)
-  const int item0 = xcd_item(B * tiles * nch * parts);
+  // spread = 0: a request's blocks share an XCD (and its q in L2); spread = 1: items go
+  // round-robin over the XCDs, which balances requests of very different sizes
+  const int total = B * tiles * nch * parts;
+  const int item0 = spread ? (static_cast<int>(blockIdx.x) < total ? static_cast<int>(blockIdx.x) : -1)
+                           : xcd_item(total);
   if (item0 < 0) return;
   const int part = item0 % parts, item = item0 / parts;
   const int b = item / (tiles * nch);
@@ -457,7 +462,8 @@ __global__ __launch_bounds__(256, (KB >= 5 || NKC >= 20) ? 1 : 2) void score_bf1
 __global__ __launch_bounds__(256) void score_bf16_any_kernel(
     int B, const int64_t* __restrict__ mem_off, int64_t n_mem, int m_max,
     const int32_t* __restrict__ node_off, int n_nodes, int t_max, const bf16_t* __restrict__ keys,
-    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S, int /*parts: 1*/) {
+    int d_m, const bf16_t* __restrict__ q, float scale, float* __restrict__ S, int /*parts: 1*/,
+    int /*spread*/) {
   using namespace score_cfg;
   constexpr int KT = 64;
   __shared__ __align__(16) bf16_t ks[KT][LDK];
