@@ -778,18 +778,33 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   // keys, valid count, max
   int cnt = 0;
   uint32_t kmax = 0;
-  for (int i = tid; i < M; i += NT) {
-    const bool v = a.valid == nullptr || a.valid[m0 + i] != 0;
-    float sc = srow[i], ps[kScoreMaxParts - 1];
+  // four entries per thread and step, every load issued before the first use
+  for (int i0 = tid; i0 < M; i0 += 4 * NT) {
+    float sc[4], ps[4][kScoreMaxParts - 1];
+    bool v[4];
 #pragma unroll
-    for (int p = 1; p < kScoreMaxParts; ++p) ps[p - 1] = p < a.s_parts ? srow[p * a.s_stride + i] : 0.f;
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * NT;
+      const bool in = i < M;
+      sc[u] = in ? srow[i] : 0.f;
 #pragma unroll
-    for (int p = 1; p < kScoreMaxParts; ++p)
-      if (p < a.s_parts) sc += ps[p - 1];
-    const uint32_t k = v ? order_key(sc) : 0u;
-    skey[i] = k;
-    cnt += v ? 1 : 0;
-    kmax = max(kmax, k);
+      for (int p = 1; p < kScoreMaxParts; ++p)
+        ps[u][p - 1] = in && p < a.s_parts ? srow[p * a.s_stride + i] : 0.f;
+      v[u] = in && (a.valid == nullptr || a.valid[m0 + i] != 0);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * NT;
+      if (i < M) {
+#pragma unroll
+        for (int p = 1; p < kScoreMaxParts; ++p)
+          if (p < a.s_parts) sc[u] += ps[u][p - 1];
+        const uint32_t k = v[u] ? order_key(sc[u]) : 0u;
+        skey[i] = k;
+        cnt += v[u] ? 1 : 0;
+        kmax = max(kmax, k);
+      }
+    }
   }
   const int nV = block_sum_int<NT>(cnt, ired);
   kmax = block_max_u32<NT>(kmax, ured);
@@ -816,10 +831,21 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
       for (int shift = 24; shift >= 0; shift -= 8) {
         hist[tid] = 0;
         __syncthreads();
+        // a thread's keys mostly share a digit: one atomic per run of equal digits
+        int cur = -1, run = 0;
         for (int i = tid; i < M; i += NT) {
           const uint32_t k = skey[i];
-          if (k != 0u && (k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
+          if (k != 0u && (k & pmask) == prefix) {
+            const int dg = static_cast<int>((k >> shift) & 255u);
+            if (dg != cur) {
+              if (run > 0) atomicAdd(&hist[cur], run);
+              cur = dg;
+              run = 0;
+            }
+            ++run;
+          }
         }
+        if (run > 0) atomicAdd(&hist[cur], run);
         __syncthreads();
         if (tid < 64) radix_pick(hist, krem, &pick);
         __syncthreads();
