@@ -185,6 +185,68 @@ __global__ __launch_bounds__(256) void corr2_combine_kernel(Corr2Epi<T> epi, Cor
                  RowPart{epi.n, n_parts(epi.d), static_cast<int>(blockIdx.x), ca.rms_part});
 }
 
+// Split-K layer 2 and the RMSNorm in one pass, one 256-thread block per row (d at most
+// 8192: thread t owns the 8-column groups 8 t + 2048 j, j < 4): the ks partials are added
+// in slice order, h' = h + g (c + b_c2) as in Corr2Epi, the sum of squares of h' is
+// reduced over the block, and h_out = T(h') / sqrt(mean(h'^2) + eps) * w.
+constexpr int kCorr2RmsMaxD = 8 * 256 * 4;
+
+template <typename T>
+__global__ __launch_bounds__(256) void corr2_rms_kernel(Corr2Epi<T> epi, Corr2Args ca, int ks,
+                                                        const float* __restrict__ part,
+                                                        const float* __restrict__ w, float eps) {
+  __shared__ float sg[1];
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  stage_gates(ca, epi.n, row, 1, true, sg);
+  __syncthreads();
+  const float g = sg[0];
+  const int n = epi.n, d = epi.d;
+  float hp[4][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col0 = 8 * static_cast<int>(threadIdx.x) + 2048 * j;
+    if (col0 < d) {
+      float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int y0 = 0; y0 < ks; y0 += 4) {
+        float t[4][8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (y0 + u < ks) load8(part + (static_cast<int64_t>(y0 + u) * n + row) * d + col0, t[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (y0 + u < ks)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += t[u][e];
+      }
+      float hv[8], b[8];
+      load8(epi.h + static_cast<int64_t>(row) * d + col0, hv);
+      load8(epi.b_c2 + col0, b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hp[j][e] = fmaf(g, v[e] + b[e], hv[e]);
+        ss = fmaf(hp[j][e], hp[j][e], ss);
+      }
+    }
+  }
+  ss = wave_sum_f32(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float rstd = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / static_cast<float>(d) + eps);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col0 = 8 * static_cast<int>(threadIdx.x) + 2048 * j;
+    if (col0 < d) {
+      float wv[8], o[8];
+      load8(w + col0, wv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = Elem<T>::to_f32(Elem<T>::from_f32(hp[j][e])) * rstd * wv[e];
+      store8(epi.h_out + static_cast<int64_t>(row) * d + col0, o);
+    }
+  }
+}
+
 // RMSNorm of h' in place: h_out = h' / sqrt(mean(h'^2) + eps) * w, one wave per row,
 // 16-byte accesses (8 consecutive columns per lane and step); d is a multiple of 64.
 template <typename T>

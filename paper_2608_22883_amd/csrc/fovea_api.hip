@@ -521,6 +521,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   }
   // 6. correction layer 2, gate, residual (+ RMS partials)
   T* h_out = static_cast<T*>(a.h_out);
+  bool fused_rms = false;
   {
     using C = Corr2Cfg<T>;
     const TileMap tm = make_tile_map((a.n + C::BM - 1) / C::BM, (D.d + C::BN - 1) / C::BN,
@@ -539,15 +540,24 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     ca.b_g2 = c->b_g2;
     ca.gate_out = a.gate_out;
     ca.rms_part = c->rms_w ? rms_part : nullptr;
-    ProfScope ps(c, kCorr2, s);
-    hipLaunchKernelGGL(corr2_kernel<T>, dim3(tile_grid(tm), ksp.c2), dim3(C::NT), 0, s, tm, a_c,
-                       static_cast<const T*>(c->W_c2), epi, ca, ksp.c2, splitk);
-    if (ksp.c2 > 1)
-      hipLaunchKernelGGL(corr2_combine_kernel<T>, dim3((D.d + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
-                         epi, ca, ksp.c2, static_cast<const float*>(splitk));
+    // split-K with the RMSNorm: the slices' sum, the residual and the norm in one pass
+    fused_rms = ksp.c2 > 1 && c->rms_w != nullptr && D.d <= kCorr2RmsMaxD;
+    {
+      ProfScope ps(c, kCorr2, s);
+      hipLaunchKernelGGL(corr2_kernel<T>, dim3(tile_grid(tm), ksp.c2), dim3(C::NT), 0, s, tm, a_c,
+                         static_cast<const T*>(c->W_c2), epi, ca, ksp.c2, splitk);
+      if (ksp.c2 > 1 && !fused_rms)
+        hipLaunchKernelGGL(corr2_combine_kernel<T>, dim3((D.d + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
+                           epi, ca, ksp.c2, static_cast<const float*>(splitk));
+    }
+    if (fused_rms) {
+      ProfScope ps(c, kRms, s);
+      hipLaunchKernelGGL(corr2_rms_kernel<T>, dim3(a.n), dim3(256), 0, s, epi, ca, ksp.c2,
+                         static_cast<const float*>(splitk), c->rms_w, D.rms_eps);
+    }
   }
   // 7. RMSNorm
-  if (c->rms_w) {
+  if (c->rms_w && !fused_rms) {
     ProfScope ps(c, kRms, s);
     hipLaunchKernelGGL(rms_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, D.d, rms_part, c->rms_w,
                        D.rms_eps, h_out);
