@@ -249,13 +249,18 @@ def test_host_argument_errors(lib):
     fv.close()
 
 
-@pytest.mark.parametrize("B,M,d_m", [(32, 576, 1024), (40, 576, 1024), (3, 130, 384), (5, 700, 896)],
-                         ids=["80-key-blocks", "96-key-blocks", "fallback-d384", "64-key-blocks-d896"])
-def test_score_tilings(lib, B, M, d_m):
-    """Each score-kernel tiling (keys per block chosen from the grid size) and the
-    unpipelined fallback agree with the oracle."""
+@pytest.mark.parametrize("B,M,d_m,M_lo", [(32, 576, 1024, None), (40, 576, 1024, None),
+                                          (3, 130, 384, None), (5, 700, 896, None),
+                                          (2, 576, 1024, None), (2, 576, 1024, 64)],
+                         ids=["80-key-blocks", "96-key-blocks", "fallback-d384", "64-key-blocks-d896",
+                              "2-k-slices", "2-k-slices-ragged-spread"])
+def test_score_tilings(lib, B, M, d_m, M_lo):
+    """Each score-kernel tiling (keys per block chosen from the grid size), the
+    unpipelined fallback, d_m split in k slices (two requests: 72 blocks, two slices)
+    and, for ragged memories, tiles spread over the XCDs agree with the oracle."""
+    extra = {} if M_lo is None else dict(M_lo=M_lo)
     wl = WORKLOADS["llava_b1"].with_(B=B, M=M, d=512, d_m=d_m, T=5, tau=0.7, tau_hi=0.95,
-                                     key_scale=(40.0, 200.0))
+                                     key_scale=(40.0, 200.0), **extra)
     case = make_case(wl, affine="random")
     g, st, _ = _run(lib, case)
     assert st == 0
