@@ -253,7 +253,7 @@ def test_host_argument_errors(lib):
                                           (3, 130, 384, None), (5, 700, 896, None),
                                           (2, 576, 1024, None), (2, 576, 1024, 64)],
                          ids=["80-key-blocks", "96-key-blocks", "fallback-d384", "64-key-blocks-d896",
-                              "2-k-slices", "2-k-slices-ragged-spread"])
+                              "2-k-slices", "k-slices-ragged-spread"])
 def test_score_tilings(lib, B, M, d_m, M_lo):
     """Each score-kernel tiling (keys per block chosen from the grid size), the
     unpipelined fallback, d_m split in k slices (two requests: 72 blocks, two slices)
