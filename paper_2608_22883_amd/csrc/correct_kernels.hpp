@@ -10,8 +10,8 @@ namespace fovea {
 
 template <typename T>
 using Corr1Cfg = GemmCfg<T, 64, 4>;
-template <typename T>
-using Corr2Cfg = GemmCfg<T, 128, 2>;
+template <typename T, int BM = 128>
+using Corr2Cfg = GemmCfg<T, BM, 2>;
 template <typename T>
 using MemCfg = GemmCfg<T, 128, 4>;
 constexpr int kPartCols = 128;  // columns reduced into one partial sum (one block tile)
@@ -147,11 +147,11 @@ __device__ __forceinline__ void stage_gates(const Corr2Args& ca, int n, int m0, 
   }
 }
 
-template <typename T>
+template <typename T, int BM = 128>
 __global__ __launch_bounds__(256) void corr2_kernel(TileMap tm, const T* __restrict__ a_c,
                                                     const T* __restrict__ Wc2, Corr2Epi<T> epi,
                                                     Corr2Args ca, int ks, float* __restrict__ part) {
-  using C = Corr2Cfg<T>;
+  using C = Corr2Cfg<T, BM>;
   static_assert(C::SMEM_BYTES >= C::OUT_BYTES + C::BM * 4, "gate staging");
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;

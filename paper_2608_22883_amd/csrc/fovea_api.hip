@@ -401,8 +401,9 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     epi.P = P;
     const int ks = ksp.hq;
     ProfScope ps(c, kHq, s);
-    hipLaunchKernelGGL(hq_kernel<T>, dim3(tile_grid(tm), ks), dim3(C::NT), 0, s, tm, a.n, h, D.d,
-                       static_cast<const T*>(c->W_hq), epi, ks, splitk);
+    // at most 64 rows: the same single row of tiles in 64-row tiles (no clamped rows)
+    hipLaunchKernelGGL((a.n <= 64 ? hq_kernel<T, 64> : hq_kernel<T>), dim3(tile_grid(tm), ks), dim3(C::NT), 0,
+                       s, tm, a.n, h, D.d, static_cast<const T*>(c->W_hq), epi, ks, splitk);
     if (ks > 1)
       hipLaunchKernelGGL(hq_combine_kernel<T>, dim3((N + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
                          epi, ks, static_cast<const float*>(splitk));
@@ -544,8 +545,9 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     fused_rms = ksp.c2 > 1 && c->rms_w != nullptr && D.d <= kCorr2RmsMaxD;
     {
       ProfScope ps(c, kCorr2, s);
-      hipLaunchKernelGGL(corr2_kernel<T>, dim3(tile_grid(tm), ksp.c2), dim3(C::NT), 0, s, tm, a_c,
-                         static_cast<const T*>(c->W_c2), epi, ca, ksp.c2, splitk);
+      hipLaunchKernelGGL((a.n <= 64 ? corr2_kernel<T, 64> : corr2_kernel<T>), dim3(tile_grid(tm), ksp.c2),
+                         dim3(C::NT), 0, s, tm, a_c, static_cast<const T*>(c->W_c2), epi, ca, ksp.c2,
+                         splitk);
       if (ksp.c2 > 1 && !fused_rms)
         hipLaunchKernelGGL(corr2_combine_kernel<T>, dim3((D.d + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
                            epi, ca, ksp.c2, static_cast<const float*>(splitk));

@@ -199,8 +199,8 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
 // score MFMA (|q - hi - lo| <= 2^-16 |q|); fp32 storage writes q itself.
 // ---------------------------------------------------------------------------------
 
-template <typename T>
-using HqCfg = GemmCfg<T, 128, 4>;
+template <typename T, int BM = 128>
+using HqCfg = GemmCfg<T, BM, 4>;
 
 // One GEMM over the hidden states for everything that depends on h alone:
 // columns [0, d_m) are the query projection (LayerNorm folded as described above),
@@ -251,11 +251,11 @@ struct HqEpi {
 
 // ks > 1: split-K (grid.y = ks slices, fp32 partials in part), finished by
 // hq_combine_kernel with the same epilogue.
-template <typename T>
+template <typename T, int BM = 128>
 __global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __restrict__ h, int d,
                                                  const T* __restrict__ Whq, HqEpi<T> epi, int ks,
                                                  float* __restrict__ part) {
-  using C = HqCfg<T>;
+  using C = HqCfg<T, BM>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;
