@@ -146,6 +146,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(int n, int d, int d_m,
                                                        float* __restrict__ xe,
                                                        float* __restrict__ y) {
   const int row = blockIdx.x;
+  if (row >= n) return;
   const bool ok = node_req[row] >= 0;
   const float2 st = stats[row];
   const int l = min(max(depth[row], 0), n_depth - 1);
@@ -181,6 +182,7 @@ __global__ __launch_bounds__(256) void bwd_sel_fwd_kernel(int n, int d, int d_m,
   __shared__ float red[4];
   __shared__ int sbad;
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (row >= n) return;
   const NodeInfo ni = info[row];
   int K = K_in[row];
   if (tid == 0) sbad = 0;
@@ -251,6 +253,7 @@ __global__ __launch_bounds__(256) void bwd_rms_gate_kernel(int n, int d, int d_c
                                                            float* __restrict__ dz) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
+  if (row >= n) return;
   const bool ok = ok_in[row] != 0;
   const int64_t ro = static_cast<int64_t>(row) * d;
   const int64_t zo = static_cast<int64_t>(row) * 2 * d_c;
@@ -315,6 +318,7 @@ __global__ __launch_bounds__(256) void bwd_sel_kernel(int n, int d_m, int k_max,
   float* sds = smem_f + d_m;  // da, then ds [k_max]
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (row >= n) return;
   const int K = ok_in[row] ? K_in[row] : 0;
   const int64_t m0 = info[row].m0;
   const int32_t* ix = idx + static_cast<int64_t>(row) * k_max;
@@ -504,6 +508,7 @@ __global__ __launch_bounds__(256) void bwd_ln_kernel(int n, int d, const float* 
                                                      float* __restrict__ dh) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
+  if (row >= n) return;
   const int64_t ro = static_cast<int64_t>(row) * d;
   float s1 = 0.f, s2 = 0.f;
   #pragma unroll 8
@@ -531,6 +536,7 @@ __global__ __launch_bounds__(256) void ln_apply_kernel(int n, int d, const float
                                                        float* __restrict__ xhat,
                                                        float* __restrict__ xn) {
   const int row = blockIdx.x;
+  if (row >= n) return;
   const float2 st = stats[row];
   const int64_t ro = static_cast<int64_t>(row) * d;
 #pragma unroll 8
