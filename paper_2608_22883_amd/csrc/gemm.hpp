@@ -419,14 +419,14 @@ __device__ __forceinline__ void splitk_combine(int M, int N, int ks, const float
   const int col0 = static_cast<int>(blockIdx.x) * 128 + static_cast<int>(threadIdx.x & 15) * 8;
   float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (row < M && col0 < N) {
-    // four slices' loads in flight at a time, added in slice order
-    for (int y0 = 0; y0 < ks; y0 += 4) {
-      float t[4][8];
+    // eight slices' loads in flight at a time, added in slice order
+    for (int y0 = 0; y0 < ks; y0 += 8) {
+      float t[8][8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
         if (y0 + u < ks) load8(part + (static_cast<int64_t>(y0 + u) * M + row) * N + col0, t[u]);
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
         if (y0 + u < ks)
 #pragma unroll
           for (int e = 0; e < 8; ++e) v[e] += t[u][e];
