@@ -113,6 +113,20 @@ def test_gate_zero_returns_h_exactly(lib, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [256, 8256])
+def test_small_batch_layer2_and_rmsnorm(lib, dtype, d):
+    """A few nodes run layer 2 split-K; with the RMSNorm, rows up to 8192 wide take the
+    one-pass combine + RMSNorm kernel and wider rows the combine and RMSNorm launches."""
+    wl = _small(dtype, d=d)
+    case = make_case(wl, affine="random")
+    g, st, _ = _run(lib, case)
+    assert st == 0
+    rep = {}
+    compare(case, g, run_oracle(case), H_TOL[dtype], rep)
+    assert rep["exempt"] <= max(2, 0.01 * rep["n"])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_gate_one_without_rmsnorm(lib, dtype):
     wl = _small(dtype)
     case = make_case(wl, affine="random")
