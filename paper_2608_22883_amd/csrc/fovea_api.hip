@@ -487,9 +487,8 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
 #undef FOVEA_SEL
 #undef FOVEA_SEL_C
     } else {
-      // the order keys, later reused for the gather's partial sums (3 x 64 lanes x VEC)
-      const size_t sel_smem = std::max(static_cast<size_t>(a.m_max) * 4,
-                                       static_cast<size_t>(3 * 64 * VEC * 4));
+      // the order keys (later the gather's partial sums) and the candidate arrays
+      const size_t sel_smem = static_cast<size_t>(select_gather_smem(a.m_max, a.k_max, VEC));
       FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
                                     hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(sel_smem)));

@@ -704,6 +704,18 @@ __device__ __forceinline__ RadixPick radix_pick(int* hist, int krem, RadixPick* 
   return *out;
 }
 
+// Dynamic LDS of select_gather_kernel: the order keys (or the gather's partial sums,
+// 3 x 64 lanes x VEC floats, whichever is larger; 8-byte aligned end), then the candidate
+// keys (8 B), prefix masses (8 B), weights (4 B) and indices (4 B) of kcap slots.
+__host__ __device__ inline int select_kcap(int k_max) { return (k_max + 3) & ~3; }
+__host__ __device__ inline int select_key_bytes(int m_max, int vec) {
+  const int b = m_max * 4 > 3 * 64 * vec * 4 ? m_max * 4 : 3 * 64 * vec * 4;
+  return (b + 7) & ~7;
+}
+__host__ __device__ inline int select_gather_smem(int m_max, int k_max, int vec) {
+  return select_key_bytes(m_max, vec) + select_kcap(k_max) * 24;
+}
+
 // Sorts the C distinct keys of list descending in place: the rank of a key is the number
 // of keys above it, counted in one broadcast pass over the list (thread tid ranks the
 // keys at tid + NT q, q < Q).
@@ -732,12 +744,18 @@ __device__ __forceinline__ void rank_sort_desc(unsigned long long* list, int C, 
 template <typename T>
 __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   constexpr int NT = 256;
-  extern __shared__ uint32_t skey[];  // [m_max] order keys; 0 marks a masked entry
+  // dynamic LDS (select_gather_smem): the order keys [m_max] (0 marks a masked entry;
+  // later the gather's partial sums), then the candidate arrays sized for k_max, so that
+  // two blocks share a compute unit even at 16384 keys
+  extern __shared__ __align__(16) unsigned char sel_smem[];
+  uint32_t* skey = reinterpret_cast<uint32_t*>(sel_smem);
+  const int kcap = select_kcap(a.k_max);
+  unsigned long long* cand =
+      reinterpret_cast<unsigned long long*>(sel_smem + select_key_bytes(a.m_max, Elem<T>::kPer16B));
+  double* pre = reinterpret_cast<double*>(cand + kcap);
+  float* alpha = reinterpret_cast<float*>(pre + kcap);
+  int* sidx = reinterpret_cast<int*>(alpha + kcap);
   __shared__ int hist[256];
-  __shared__ unsigned long long cand[kMaxKmax];
-  __shared__ double pre[kMaxKmax];
-  __shared__ float alpha[kMaxKmax];
-  __shared__ int sidx[kMaxKmax];
   __shared__ int ired[NT / 64];
   __shared__ double dred[NT / 64];
   __shared__ uint32_t ured[NT / 64];
@@ -887,7 +905,7 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
                         (k == thr && (all_eq || 0xFFFFu - static_cast<uint32_t>(i) >= thr_inv));
       if (take) {
         const int pos = atomicAdd(&s_count, 1);
-        if (pos < kMaxKmax)
+        if (pos < kcap)
           cand[pos] = (static_cast<unsigned long long>(k) << 32) |
                       static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(i));
       }
@@ -931,7 +949,7 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int t = 4 * tid + j;
-        if (t < kMaxKmax) pre[t] = off + e4[j];
+        if (t < kcap) pre[t] = off + e4[j];
       }
     }
     if (tid == 0) s_first = INT_MAX;
