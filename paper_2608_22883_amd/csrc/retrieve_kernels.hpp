@@ -1300,7 +1300,8 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
       return K;
     }
     {
-      // larger candidate sets: bitonic sort in LDS, then the prefix
+      // larger candidate sets: bitonic sort in LDS, then the prefix (masses from the same
+      // hardware exp2 as Z, so that the prefix never exceeds Z by a differing rounding)
       int P = 128;
       while (P < C) P <<= 1;
       for (int i = Cc + lane; i < P; i += 64) cand[i] = 0ull;
@@ -1325,7 +1326,7 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int t = 4 * lane + u;
-        e4[u] = t < C ? static_cast<double>(expf(key_to_float(static_cast<uint32_t>(cand[t] >> 32)) - smax)) : 0.0;
+        e4[u] = t < C ? static_cast<double>(__builtin_amdgcn_exp2f((key_to_float(static_cast<uint32_t>(cand[t] >> 32)) - smax) * kLog2e)) : 0.0;
         loc += e4[u];
         e4[u] = loc;
       }
@@ -1352,7 +1353,7 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
     mass = sumI / Z;
     for (int t = lane; t < K; t += 64) {
       const unsigned long long x = cand[t];
-      const float et = expf(key_to_float(static_cast<uint32_t>(x >> 32)) - smax);
+      const float et = __builtin_amdgcn_exp2f((key_to_float(static_cast<uint32_t>(x >> 32)) - smax) * kLog2e);
       alpha_o[t] = static_cast<float>(static_cast<double>(et) / sumI);
       idx_o[t] = static_cast<int>(min(0xFFFFFFFFu - static_cast<uint32_t>(x), static_cast<uint32_t>(M - 1)));
     }

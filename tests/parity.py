@@ -1,18 +1,18 @@
 """Helpers shared by the GPU parity tests: move a synthetic case to the device, run the
 library through its C ABI, run the oracle on the same rounded inputs, and compare.
 
-Index sets are compared exactly.  A node is exempt from exact comparison only when the
-oracle's own decision is ambiguous at the precision the library computes scores in:
-  * mass band: |C_K - tau| or |C_{K-1} - tau| below DELTA_C(node), where a score
-    error of delta_s moves any prefix mass by at most 2 delta_s;
-  * tie band: the oracle scores ranked K and K+1 differ by less than 2 delta_s.
-delta_s(node) = SCORE_REL * max_i sum_m |q_m k_im| / sqrt(d_m) bounds the fp32 error of
-the score dot products (condition number times the unit roundoff, with headroom);
-DELTA_C = max(1e-6, 2 delta_s).  For exempt nodes the library's answer must still be
-valid: a top-K set of the oracle scores up to 2 delta_s, whose K obeys the rule up to
-DELTA_C; its readout and hidden state are compared with the oracle re-run on that set.
-Within a matched set, adjacent ranks may swap only where their oracle scores are
-within 2 delta_s.
+Index sets (rank order, ``idx_out[:K]``) must equal the oracle's.  A node may differ
+only where the oracle's own decision is ambiguous at a fixed, stated precision:
+  * mass band (the rule of the workloads' specification): the oracle's prefix mass
+    C_K or C_{K-1} lies within MASS_BAND = 1e-6 of tau;
+  * tie band: the oracle's scores ranked K and K+1 differ by less than
+    tie_band(s_K) = 1e-5 max(1, |s_K|).
+Inside a set that matches, two ranks may hold each other's entries only where their
+oracle scores are within the tie band.  For a node that differs, the library's answer
+must still be the oracle's answer with tied entries exchanged or K moved by one rank
+across tau; its readout and hidden state are compared with the oracle re-run on the
+library's set.  Every comparison fills a report (exempt and swapped counts, how many
+nodes the bands admit at all, the largest errors) that the session prints at its end.
 """
 
 from __future__ import annotations
@@ -24,7 +24,15 @@ import torch
 
 import oracle
 
-SCORE_REL = 2.0 ** -19  # ~1.9e-6: fp32 dot products of length <= 4096 with fp32 q
+MASS_BAND = 1e-6
+TIE_REL = 1e-5
+
+# reports of every compare() call in this session, printed by conftest's terminal summary
+REPORTS: list = []
+
+
+def tie_band(s):
+    return TIE_REL * max(1.0, abs(float(s)))
 
 
 def to_device(case, dtype_name: str, device="cuda"):
@@ -65,20 +73,21 @@ def gpu_outputs(out):
                 mass=out.mass.double().cpu().numpy(), r=out.r.double().cpu().numpy())
 
 
-def _delta_s(case, ref, node, b):
-    m0, m1 = int(case.mem_off[b]), int(case.mem_off[b + 1])
-    if m1 == m0:
-        return 0.0
-    k = np.abs(case.keys[m0:m1])
-    q = np.abs(ref["q"][node])
-    return SCORE_REL * float((k @ q).max()) / math.sqrt(case.keys.shape[1])
+
+def _in_band(rec, Ko, tau):
+    """(mass, tie): is the oracle's decision at node record `rec` ambiguous?"""
+    prefix, order, s = rec["prefix"], rec["order"], rec["s"]
+    near_mass = any(1 <= t <= len(prefix) and abs(prefix[t - 1] - tau) < MASS_BAND for t in (Ko - 1, Ko))
+    near_tie = (0 < Ko < len(order)) and abs(s[order[Ko - 1]] - s[order[Ko]]) < tie_band(s[order[Ko - 1]])
+    return near_mass, near_tie
 
 
-def compare(case, g, ref, h_tol: float, report: dict | None = None, weights: dict | None = None):
+def compare(case, g, ref, h_tol: float, report: dict | None = None, weights: dict | None = None,
+            label: str | None = None):
     """Assert parity of library outputs ``g`` (dict of numpy arrays) with oracle ``ref``."""
     n = case.n_nodes
     node_b = np.repeat(np.arange(len(case.node_off) - 1), np.diff(case.node_off))
-    exempt, swapped = [], 0
+    exempt, swapped, admissible = [], 0, 0
     r_ref = ref["r"].copy()
     need_rerun = []
     for node in range(n):
@@ -90,44 +99,40 @@ def compare(case, g, ref, h_tol: float, report: dict | None = None, weights: dic
         if rec is None:
             assert Kg == 0
             continue
-        ds = _delta_s(case, ref, node, b)
-        dC = max(1e-6, 2 * ds)
         s = rec["s"]
         order, prefix = rec["order"], rec["prefix"]
         tau = float(case.tau[b])
+        near_mass, near_tie = _in_band(rec, Ko, tau)
+        admissible += int(near_mass or near_tie)
         if Kg == Ko and np.array_equal(np.sort(io), np.sort(ig)):
             if not np.array_equal(io, ig):
-                # order differs: only adjacent near-ties may swap
-                pos = {int(i): t for t, i in enumerate(io)}
+                # order differs: only entries whose oracle scores are tied may trade ranks
                 for t, i in enumerate(ig):
-                    assert abs(s[i] - s[io[t]]) <= 2 * ds, (
+                    assert abs(s[i] - s[io[t]]) <= tie_band(s[io[t]]), (
                         f"node {node}: rank {t} holds {i} (s={s[i]!r}) instead of {io[t]} "
-                        f"(s={s[io[t]]!r}), beyond the tie band {2 * ds:.3g}")
-                    assert abs(pos[int(i)] - t) <= 8
+                        f"(s={s[io[t]]!r}), beyond the tie band {tie_band(s[io[t]]):.3g}")
                 swapped += 1
             continue
         # sets differ: the oracle decision must be ambiguous ...
-        near_mass = any(0 < t <= len(prefix) and abs(prefix[t - 1] - tau) < dC
-                        for t in (Ko - 1, Ko, Ko + 1))
-        near_tie = Ko < len(order) and abs(s[order[Ko - 1]] - s[order[Ko]]) < 2 * ds if Ko > 0 else False
         assert near_mass or near_tie, (
             f"node {node} (request {b}): K gpu={Kg} oracle={Ko}; sets differ but the oracle "
-            f"decision is not ambiguous (delta_s={ds:.3g}, C_K={prefix[Ko - 1]!r}, tau={tau!r}, "
-            f"gap={s[order[Ko - 1]] - s[order[Ko]] if Ko < len(order) else None!r})")
-        # ... and the library's answer valid up to the same bands
+            f"decision is not ambiguous (C_K - tau = {prefix[Ko - 1] - tau!r}, "
+            f"C_K-1 - tau = {prefix[Ko - 2] - tau if Ko > 1 else None!r}, "
+            f"score gap at K = {s[order[Ko - 1]] - s[order[Ko]] if Ko < len(order) else None!r})")
+        # ... and the library's answer the oracle's, up to what the band allows
         nV, k_max, k_min = rec["n_valid"], case.k_max, case.k_min
         assert 1 <= Kg <= min(nV, k_max) and Kg >= min(k_min, nV)
-        sK = np.sort(s[ig])[0]
-        assert (s[order[:Kg]] >= sK - 2 * ds).all() and (s[ig] >= s[order[Kg - 1]] - 2 * ds).all()
-        at = rec["alpha_tilde"]
-        Vidx = np.flatnonzero(np.ones(len(s), bool) if case.valid is None
-                              else case.valid[int(case.mem_off[b]):int(case.mem_off[b + 1])])
-        pos_of = {int(v): j for j, v in enumerate(Vidx)}
-        mass_g = sum(at[pos_of[int(i)]] for i in ig)
-        if Kg not in (k_max, nV) and Kg > k_min:
-            assert mass_g >= tau - dC, f"node {node}: gpu set mass {mass_g} < tau {tau}"
-        if Kg > max(k_min, 1):
-            assert prefix[Kg - 2] < tau + dC, f"node {node}: gpu K={Kg} is not minimal"
+        if near_tie and Kg == Ko:
+            # the same ranks with tied entries exchanged: equal score profiles up to the band
+            so, sg = np.sort(s[io])[::-1], np.sort(s[ig])[::-1]
+            assert all(abs(a - c) <= tie_band(a) for a, c in zip(so, sg)), f"node {node}: not a tie swap"
+        else:
+            assert near_mass and abs(Kg - Ko) == 1, f"node {node}: K moved by {Kg - Ko}"
+            m = min(Kg, Ko)
+            so, sg = s[order[:m]], s[(ig if Kg > Ko else io)[:m]]
+            assert np.array_equal(np.sort(ig[:m]), np.sort(io[:m])) or all(
+                abs(a - c) <= tie_band(a) for a, c in zip(np.sort(so), np.sort(sg))), \
+                f"node {node}: K moved across tau but the common ranks differ"
         exempt.append(node)
         need_rerun.append((node, b, ig))
     # oracle readout and correction on the library's set for exempt nodes
@@ -142,21 +147,24 @@ def compare(case, g, ref, h_tol: float, report: dict | None = None, weights: dic
                                   W["b_c2"], W["W_g1"], W["b_g1"], W["w_g2"], W["b_g2"])
         h_ref[rows] = oracle.fuse(case.h[rows], gt, c, W.get("rms_w"), W["rms_eps"])
     # floating-point outputs
-    live = np.array([ref["records"][i] is not None for i in range(n)])
+    live = np.array([ref["records"][i] is not None for i in range(n)], dtype=bool)
     rel = np.linalg.norm(g["h_out"] - h_ref, axis=1) / np.maximum(np.linalg.norm(h_ref, axis=1), 1e-300)
     assert np.isfinite(g["h_out"]).all()
     worst = int(np.argmax(rel))
-    assert rel.max() <= h_tol, f"h_out rel err {rel.max():.3e} > {h_tol} at node {worst}"
     rr = np.linalg.norm(g["r"] - r_ref, axis=1) / np.maximum(np.linalg.norm(r_ref, axis=1), 1e-30)
     r_tol = 1e-4 if case.workload.dtype == "f32" else 1e-3
-    assert rr[live].max(initial=0) <= r_tol, f"r rel err {rr.max():.3e} at node {int(np.argmax(rr))}"
-    same = np.setdiff1d(np.arange(n), exempt)
-    if len(same):
-        dm = np.abs(g["mass"][same] - ref["mass"][same])
-        assert dm.max() <= 1e-4, f"mass err {dm.max():.3e}"
+    same = np.setdiff1d(np.flatnonzero(live), exempt)
+    dm = np.abs(g["mass"][same] - ref["mass"][same]) if len(same) else np.zeros(1)
     ge = np.abs(g["gate"] - ref["gate"])
-    assert ge.max() <= (1e-5 if case.workload.dtype == "f32" else 5e-3), f"gate err {ge.max():.3e}"
+    rep = dict(label=label or case.workload.name, n=n, exempt=len(exempt), swapped=swapped,
+               admissible=admissible, h_rel_max=float(rel.max(initial=0)),
+               r_rel_max=float(rr[live].max(initial=0)), mass_err_max=float(dm.max(initial=0)),
+               gate_err_max=float(ge.max(initial=0)))
+    REPORTS.append(rep)
     if report is not None:
-        report.update(exempt=len(exempt), swapped=swapped, n=n, h_rel_max=float(rel.max()),
-                      r_rel_max=float(rr[live].max(initial=0)))
+        report.update(rep)
+    assert rel.max() <= h_tol, f"h_out rel err {rel.max():.3e} > {h_tol} at node {worst}"
+    assert rr[live].max(initial=0) <= r_tol, f"r rel err {rr.max():.3e} at node {int(np.argmax(rr))}"
+    assert dm.max(initial=0) <= 1e-4, f"mass err {dm.max():.3e}"
+    assert ge.max() <= (1e-5 if case.workload.dtype == "f32" else 5e-3), f"gate err {ge.max():.3e}"
     return exempt

@@ -58,9 +58,9 @@ def test_workload_parity(lib, name, affine):
     assert st == 0, f"data error bits {bits:#x}"
     ref = run_oracle(case)
     rep = {}
-    compare(case, g, ref, H_TOL[wl.dtype], rep)
+    compare(case, g, ref, H_TOL[wl.dtype], rep, label=f"{name}/{affine}")
     print(f"[gpu] {name}/{affine}: {rep}", flush=True)
-    assert rep["exempt"] <= max(2, 0.01 * rep["n"])
+    assert rep["exempt"] <= rep["admissible"]
 
 
 def _small(dtype="f32", **kw):
@@ -75,7 +75,7 @@ def test_dense_tau_one(lib, dtype):
     g, st, _ = _run(lib, case)
     ref = run_oracle(case)
     assert (g["K"] == 200).all() and (ref["K"] == 200).all()
-    compare(case, g, ref, H_TOL[dtype])
+    compare(case, g, ref, H_TOL[dtype], label=f"dense tau=1 {dtype}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -121,9 +121,7 @@ def test_small_batch_layer2_and_rmsnorm(lib, dtype, d):
     case = make_case(wl, affine="random")
     g, st, _ = _run(lib, case)
     assert st == 0
-    rep = {}
-    compare(case, g, run_oracle(case), H_TOL[dtype], rep)
-    assert rep["exempt"] <= max(2, 0.01 * rep["n"])
+    compare(case, g, run_oracle(case), H_TOL[dtype], label=f"small-batch layer 2 {dtype} d={d}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -134,7 +132,7 @@ def test_gate_one_without_rmsnorm(lib, dtype):
     g, st, _ = _run(lib, case, W=W)
     ref = run_oracle(case, weights=W)
     assert (g["gate"] == 1).all()
-    compare(case, g, ref, H_TOL[dtype], weights=W)
+    compare(case, g, ref, H_TOL[dtype], weights=W, label=f"gate one, no RMSNorm {dtype}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -144,7 +142,7 @@ def test_cardinality_bounds(lib, dtype, k_min, k_max):
     case = make_case(wl, affine="random")
     g, _, _ = _run(lib, case)
     ref = run_oracle(case)
-    compare(case, g, ref, H_TOL[dtype])
+    compare(case, g, ref, H_TOL[dtype], label=f"cardinality k_min={k_min} k_max={k_max} {dtype}")
     assert (g["K"] <= k_max).all() and (g["K"] >= min(k_min, 300)).all()
 
 
@@ -166,7 +164,7 @@ def test_masked_and_ragged_and_empty(lib, dtype):
     g, st, bits = _run(lib, case)
     assert st == 0, bits
     ref = run_oracle(case)
-    compare(case, g, ref, H_TOL[dtype])
+    compare(case, g, ref, H_TOL[dtype], label=f"masked, ragged, empty {dtype}")
     b1 = slice(case.node_off[1], case.node_off[2])
     assert (g["K"][b1] == 0).all() and (g["r"][b1] == 0).all()
     for node in range(case.n_nodes):
@@ -278,4 +276,4 @@ def test_score_tilings(lib, B, M, d_m, M_lo):
     case = make_case(wl, affine="random")
     g, st, _ = _run(lib, case)
     assert st == 0
-    compare(case, g, run_oracle(case), H_TOL["bf16"])
+    compare(case, g, run_oracle(case), H_TOL["bf16"], label=f"score tiling B={B} M={M} d_m={d_m}")
