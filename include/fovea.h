@@ -38,7 +38,8 @@
  *     context, write NaN into the affected nodes' outputs, and are read with
  *     fovea_last_error.  Nothing throws across this ABI.
  *   - Calls that share one context may run on different streams, but they share
- *     the context's error word.
+ *     the context's error word: one sticky word per context (not per workspace), so
+ *     data errors of calls on two streams are reported together.
  */
 #ifndef FOVEA_H_
 #define FOVEA_H_
@@ -115,21 +116,34 @@ const char* fovea_status_str(fovea_status s);
 /* Create a context on the current HIP device: validates dims, copies and packs the
  * weights (the query and memory LayerNorm gains are folded into W_Q and [W_K; W_U]
  * and, for bf16, the folded products are stored in bf16).  Enqueued on `stream` and
- * synchronised before returning.  *out is NULL on failure. */
+ * synchronised before returning.  The context's one allocation (the packed weights and
+ * its error word) is made here; no later call allocates device memory.  *out is NULL
+ * on failure. */
 fovea_status fovea_create(fovea_ctx** out, const fovea_dims* dims, const fovea_params* params,
                           hipStream_t stream);
+/* Waits for the last call enqueued through this context on each stream it was used on,
+ * then frees the context.  NULL is a no-op. */
 void fovea_destroy(fovea_ctx* ctx);
+
+/* Bytes of workspace fovea_build_memory needs for n_rows tokens (0 on bad arguments). */
+size_t fovea_build_memory_workspace(const fovea_ctx* ctx, int64_t n_rows);
 
 /* Memory build (Method, image-specific visual memory): for each of the n_rows visual
  * tokens V[i] ([n_rows, d_v]) write keys[i] = W_K LN(V[i]) and values[i] = W_U LN(V[i])
- * ([n_rows, d_m] each).  Rows are independent, so the memories of many images can be
- * built in one call.  keys/values must not overlap V or each other. */
+ * ([n_rows, d_m] each).  Rows are independent, so the memories of many images (a
+ * ragged batch packed by offsets) are built by one call over all of their rows; no
+ * offsets are needed.  keys/values must not overlap V, each other or the workspace.
+ * workspace: at least fovea_build_memory_workspace(ctx, n_rows) bytes, 256-byte
+ * aligned, clobbered (the rows' LayerNorm statistics). */
 fovea_status fovea_build_memory(fovea_ctx* ctx, int64_t n_rows, const void* V, void* keys,
-                                void* values, hipStream_t stream);
+                                void* values, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
-/* Bytes of workspace fovea_retrieve_fuse needs for these sizes (0 on bad arguments). */
-size_t fovea_retrieve_fuse_workspace(const fovea_ctx* ctx, int32_t n_nodes_total, int32_t m_max,
-                                     int32_t k_max);
+/* Bytes of workspace fovea_retrieve_fuse needs for a call with these sizes (0 on bad
+ * arguments): B requests, n_nodes_total nodes, n_mem_total memory rows, at most m_max
+ * rows per request, k_max. */
+size_t fovea_retrieve_fuse_workspace(const fovea_ctx* ctx, int32_t B, int32_t n_nodes_total,
+                                     int64_t n_mem_total, int32_t m_max, int32_t k_max);
 
 /* One draft step over a ragged batch of B requests (Algorithm 1, retrieval and
  * correction for every node passed).

@@ -45,8 +45,14 @@ struct fovea_ctx {
   float b_g2;
   float* rms_w;  // [d] or null
   uint32_t* err;  // sticky device-data error bits
-  float2* build_stats;
-  int64_t build_stats_rows;
+  size_t lds_limit[5];  // dynamic LDS limit of each LdsKernel
+  // one completion event per stream that calls have enqueued work on: fovea_destroy
+  // waits for these (not for the whole device) before it frees the packed weights
+  struct StreamUse {
+    hipStream_t stream;
+    hipEvent_t done;
+  };
+  std::vector<StreamUse> uses;
   // diagnostics: HIP event pairs around each launched kernel
   bool prof;
   struct ProfRec {
@@ -56,6 +62,9 @@ struct fovea_ctx {
   std::vector<ProfRec> prof_recs;
   std::vector<hipEvent_t> prof_pool;
 };
+
+// kernels whose dynamic LDS limit the context sets (raise_lds_limits)
+enum LdsKernel { kLdsSelBf16, kLdsSelF32, kLdsBwdMem, kLdsBwdSelFwd, kLdsBwdSel, kNumLdsKernels };
 
 namespace {
 
@@ -187,6 +196,39 @@ struct ProfScope {
   }
 };
 
+// Marks the end of a call's work on `s` (the event of that stream is re-recorded).
+fovea_status record_use(fovea_ctx* c, hipStream_t s) {
+  for (auto& u : c->uses)
+    if (u.stream == s) return hipEventRecord(u.done, s) == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+  hipEvent_t e = nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return FOVEA_ERR_DEVICE;
+  c->uses.push_back({s, e});
+  return hipEventRecord(e, s) == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+}
+
+// Kernels launched with a large dynamic LDS: their limit is set once, in fovea_create,
+// to what the compute unit's 160 KB leaves beside the kernel's static LDS, and kept in
+// the context for each launch to check its own size against.
+constexpr int kLdsBytes = 160 * 1024;
+
+fovea_status raise_lds_limits(fovea_ctx* c) {
+  const void* kernels[kNumLdsKernels] = {
+      reinterpret_cast<const void*>(select_gather_kernel<bf16_t>),
+      reinterpret_cast<const void*>(select_gather_kernel<float>),
+      reinterpret_cast<const void*>(bwd_mem_grad_kernel),
+      reinterpret_cast<const void*>(bwd_sel_fwd_kernel),
+      reinterpret_cast<const void*>(bwd_sel_kernel)};
+  for (int i = 0; i < kNumLdsKernels; ++i) {
+    hipFuncAttributes at;
+    FOVEA_HIP(hipFuncGetAttributes(&at, kernels[i]));
+    const int limit = kLdsBytes - static_cast<int>(at.sharedSizeBytes);
+    if (limit <= 0) return FOVEA_ERR_DEVICE;
+    FOVEA_HIP(hipFuncSetAttribute(kernels[i], hipFuncAttributeMaxDynamicSharedMemorySize, limit));
+    c->lds_limit[i] = static_cast<size_t>(limit);
+  }
+  return FOVEA_OK;
+}
+
 template <typename T>
 fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
   const fovea_dims& D = c->dims;
@@ -238,12 +280,13 @@ fovea_status pack_weights(fovea_ctx* c, const fovea_params* p, hipStream_t s) {
 }
 
 template <typename T>
-fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* values, hipStream_t s) {
+fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* values,
+                       float2* build_stats, hipStream_t s) {
   const fovea_dims& D = c->dims;
   {
     ProfScope ps(c, kMemStats, s);
     hipLaunchKernelGGL(row_stats_kernel<T>, dim3((n + 3) / 4), dim3(256), 0, s, n,
-                       static_cast<const T*>(V), D.d_v, D.ln_eps, c->build_stats,
+                       static_cast<const T*>(V), D.d_v, D.ln_eps, build_stats,
                        static_cast<const int32_t*>(nullptr), 0, static_cast<const int32_t*>(nullptr),
                        0, 0, static_cast<const float*>(nullptr),
                        static_cast<const int64_t*>(nullptr), int64_t{0}, 0,
@@ -256,7 +299,7 @@ fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* val
     ProfScope ps(c, kMemProj, s);
     hipLaunchKernelGGL(mem_proj_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, n,
                        static_cast<const T*>(V), D.d_v, static_cast<const T*>(c->W_KU), D.d_m,
-                       c->build_stats, c->m_c1, c->m_c2, static_cast<T*>(keys),
+                       build_stats, c->m_c1, c->m_c2, static_cast<T*>(keys),
                        static_cast<T*>(values));
   }
   FOVEA_HIP(hipGetLastError());
@@ -489,9 +532,8 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     } else {
       // the order keys (later the gather's partial sums) and the candidate arrays
       const size_t sel_smem = static_cast<size_t>(select_gather_smem(a.m_max, a.k_max, VEC));
-      FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(select_gather_kernel<T>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize,
-                                    static_cast<int>(sel_smem)));
+      if (sel_smem > c->lds_limit[std::is_same<T, bf16_t>::value ? kLdsSelBf16 : kLdsSelF32])
+        return FOVEA_ERR_UNSUPPORTED;
       // few nodes: each node's row is also split into column slices over several blocks
       // (each repeats the selection) so that the gathers run on more compute units
       const int cpr64 = (D.d_m / VEC + 63) / 64;
@@ -874,12 +916,9 @@ fovea_status run_backward(fovea_ctx* c, const BwdArgs& a, hipStream_t s) {
   const size_t sm_fwd = static_cast<size_t>(dm + a.k_max) * 4;
   const size_t sm_bwd = static_cast<size_t>(dm + a.k_max) * 4;
   const size_t sm_mem = static_cast<size_t>(a.t_max) * kMemRows * 2 * 4;
-  FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_mem_grad_kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_mem)));
-  FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_sel_fwd_kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_fwd)));
-  FOVEA_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(bwd_sel_kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_bwd)));
+  if (sm_mem > c->lds_limit[kLdsBwdMem] || sm_fwd > c->lds_limit[kLdsBwdSelFwd] ||
+      sm_bwd > c->lds_limit[kLdsBwdSel])
+    return FOVEA_ERR_UNSUPPORTED;
   {
     ProfScope ps(c, kBwdFill, s);
     launch_fill(F(L.tau0), a.B, s);
@@ -1184,6 +1223,7 @@ fovea_status fovea_create(fovea_ctx** out, const fovea_dims* dims, const fovea_p
   c->rms_w = p->rms_w ? reinterpret_cast<float*>(base + oRms) : nullptr;
   c->err = reinterpret_cast<uint32_t*>(base + oErr);
   fovea_status st = hipMemsetAsync(c->err, 0, 4, stream) == hipSuccess ? FOVEA_OK : FOVEA_ERR_DEVICE;
+  if (st == FOVEA_OK) st = raise_lds_limits(c);
   if (st == FOVEA_OK) st = c->bf16 ? pack_weights<bf16_t>(c, p, stream) : pack_weights<float>(c, p, stream);
   if (st == FOVEA_OK && hipStreamSynchronize(stream) != hipSuccess) st = FOVEA_ERR_DEVICE;
   if (st != FOVEA_OK) {
@@ -1200,9 +1240,12 @@ void fovea_destroy(fovea_ctx* c) {
   int cur = 0;
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(c->device);
-  (void)hipDeviceSynchronize();
+  // wait for the last call enqueued on each stream this context was used on
+  for (auto& u : c->uses) {
+    (void)hipEventSynchronize(u.done);
+    (void)hipEventDestroy(u.done);
+  }
   (void)hipFree(c->block);
-  if (c->build_stats) (void)hipFree(c->build_stats);
   for (auto& r : c->prof_recs) {
     (void)hipEventDestroy(r.e0);
     (void)hipEventDestroy(r.e1);
@@ -1212,36 +1255,41 @@ void fovea_destroy(fovea_ctx* c) {
   delete c;
 }
 
-fovea_status fovea_build_memory(fovea_ctx* c, int64_t n_rows, const void* V, void* keys,
-                                void* values, hipStream_t stream) {
-  if (c == nullptr || n_rows < 0) return FOVEA_ERR_INVALID_ARG;
-  if (n_rows == 0) return FOVEA_OK;
-  if (V == nullptr || keys == nullptr || values == nullptr) return FOVEA_ERR_INVALID_ARG;
-  if (n_rows > (int64_t{1} << 30)) return FOVEA_ERR_UNSUPPORTED;
-  if (!aligned16(V) || !aligned16(keys) || !aligned16(values)) return FOVEA_ERR_INVALID_ARG;
-  const size_t nv = static_cast<size_t>(n_rows) * c->dims.d_v * c->es;
-  const size_t nk = static_cast<size_t>(n_rows) * c->dims.d_m * c->es;
-  if (overlaps(keys, nk, V, nv) || overlaps(values, nk, V, nv) || overlaps(keys, nk, values, nk))
-    return FOVEA_ERR_INVALID_ARG;
-  if (c->build_stats_rows < n_rows) {
-    if (c->build_stats) {
-      if (hipStreamSynchronize(stream) != hipSuccess) return FOVEA_ERR_DEVICE;
-      (void)hipFree(c->build_stats);
-      c->build_stats = nullptr;
-      c->build_stats_rows = 0;
-    }
-    if (hipMalloc(&c->build_stats, static_cast<size_t>(n_rows) * sizeof(float2)) != hipSuccess)
-      return FOVEA_ERR_DEVICE;
-    c->build_stats_rows = n_rows;
-  }
-  const int n = static_cast<int>(n_rows);
-  return c->bf16 ? run_build<bf16_t>(c, n, V, keys, values, stream)
-                 : run_build<float>(c, n, V, keys, values, stream);
+size_t fovea_build_memory_workspace(const fovea_ctx* c, int64_t n_rows) {
+  if (c == nullptr || n_rows < 0) return 0;
+  return align_up(static_cast<size_t>(n_rows) * sizeof(float2)) + kAlign;
 }
 
-size_t fovea_retrieve_fuse_workspace(const fovea_ctx* c, int32_t n_nodes_total, int32_t m_max,
-                                     int32_t k_max) {
-  if (c == nullptr || n_nodes_total < 0 || m_max < 0 || k_max < 1) return 0;
+fovea_status fovea_build_memory(fovea_ctx* c, int64_t n_rows, const void* V, void* keys,
+                                void* values, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  if (c == nullptr || n_rows < 0) return FOVEA_ERR_INVALID_ARG;
+  if (n_rows == 0) return FOVEA_OK;
+  if (V == nullptr || keys == nullptr || values == nullptr || workspace == nullptr)
+    return FOVEA_ERR_INVALID_ARG;
+  if (n_rows > (int64_t{1} << 30)) return FOVEA_ERR_UNSUPPORTED;
+  if (!aligned16(V) || !aligned16(keys) || !aligned16(values)) return FOVEA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return FOVEA_ERR_WORKSPACE;
+  if (workspace_bytes < fovea_build_memory_workspace(c, n_rows)) return FOVEA_ERR_WORKSPACE;
+  const size_t nv = static_cast<size_t>(n_rows) * c->dims.d_v * c->es;
+  const size_t nk = static_cast<size_t>(n_rows) * c->dims.d_m * c->es;
+  if (overlaps(keys, nk, V, nv) || overlaps(values, nk, V, nv) || overlaps(keys, nk, values, nk) ||
+      overlaps(workspace, workspace_bytes, keys, nk) || overlaps(workspace, workspace_bytes, values, nk))
+    return FOVEA_ERR_INVALID_ARG;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
+  if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
+  const int n = static_cast<int>(n_rows);
+  float2* stats = static_cast<float2*>(workspace);
+  const fovea_status st = c->bf16 ? run_build<bf16_t>(c, n, V, keys, values, stats, stream)
+                                  : run_build<float>(c, n, V, keys, values, stats, stream);
+  return st == FOVEA_OK ? record_use(c, stream) : st;
+}
+
+size_t fovea_retrieve_fuse_workspace(const fovea_ctx* c, int32_t B, int32_t n_nodes_total,
+                                     int64_t n_mem_total, int32_t m_max, int32_t k_max) {
+  if (c == nullptr || B < 0 || n_nodes_total < 0 || n_mem_total < 0 || m_max < 0 || k_max < 1)
+    return 0;
   return ws_layout(c->dims, n_nodes_total, m_max).total;
 }
 
@@ -1302,7 +1350,8 @@ fovea_status fovea_retrieve_fuse(fovea_ctx* c, int32_t B, const int64_t* mem_off
   a.mass_out = mass_out;
   a.r_out = r_out;
   a.ws = static_cast<char*>(workspace);
-  return c->bf16 ? run_retrieve_fuse<bf16_t>(c, a, stream) : run_retrieve_fuse<float>(c, a, stream);
+  const fovea_status st = c->bf16 ? run_retrieve_fuse<bf16_t>(c, a, stream) : run_retrieve_fuse<float>(c, a, stream);
+  return st == FOVEA_OK ? record_use(c, stream) : st;
 }
 
 fovea_status fovea_last_error(fovea_ctx* c, hipStream_t stream, uint32_t* bits) {
@@ -1376,8 +1425,10 @@ fovea_status fovea_lm_topk(fovea_ctx* c, int32_t n_rows, const void* h, const vo
   if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
   if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
   uint64_t* cand = static_cast<uint64_t*>(workspace);
-  return c->bf16 ? run_lm_topk<bf16_t>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream)
-                 : run_lm_topk<float>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream);
+  const fovea_status st =
+      c->bf16 ? run_lm_topk<bf16_t>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream)
+              : run_lm_topk<float>(c, n_rows, h, W_LM, vocab, k, idx_out, logit_out, cand, stream);
+  return st == FOVEA_OK ? record_use(c, stream) : st;
 }
 
 size_t fovea_retrieve_fuse_backward_workspace(const fovea_ctx* c, int32_t B, int32_t n_nodes_total,
@@ -1471,7 +1522,8 @@ fovea_status fovea_retrieve_fuse_backward(
   a.dvalues = dvalues;
   a.G = g;
   a.ws = static_cast<char*>(workspace);
-  return run_backward(c, a, stream);
+  const fovea_status st = run_backward(c, a, stream);
+  return st == FOVEA_OK ? record_use(c, stream) : st;
 }
 
 size_t fovea_build_memory_backward_workspace(const fovea_ctx* c, int64_t n_rows) {
@@ -1512,8 +1564,9 @@ fovea_status fovea_build_memory_backward(fovea_ctx* c, const fovea_params* p, in
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return FOVEA_ERR_DEVICE;
   if (cur != c->device) return FOVEA_ERR_INVALID_ARG;
-  return run_mem_backward(c, p, static_cast<int>(n_rows), V, dkeys, dvalues, dW_K, dW_U, dmem_ln_g,
-                          dmem_ln_b, dV, static_cast<char*>(workspace), stream);
+  const fovea_status st = run_mem_backward(c, p, static_cast<int>(n_rows), V, dkeys, dvalues, dW_K, dW_U,
+                                           dmem_ln_g, dmem_ln_b, dV, static_cast<char*>(workspace), stream);
+  return st == FOVEA_OK ? record_use(c, stream) : st;
 }
 
 }  // extern "C"

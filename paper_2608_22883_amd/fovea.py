@@ -39,7 +39,8 @@ FOVEA_LM_MAX_ROWS = 1 << 20
 
 EXPORTED = [
     "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
-    "fovea_build_memory", "fovea_retrieve_fuse_workspace", "fovea_retrieve_fuse",
+    "fovea_build_memory_workspace", "fovea_build_memory", "fovea_retrieve_fuse_workspace",
+    "fovea_retrieve_fuse",
     "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
     "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward",
     "fovea_build_memory_backward_workspace", "fovea_build_memory_backward",
@@ -88,10 +89,12 @@ def _load() -> ctypes.CDLL:
     lib.fovea_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(Dims), ctypes.POINTER(Params), vp]
     lib.fovea_destroy.restype = None
     lib.fovea_destroy.argtypes = [vp]
+    lib.fovea_build_memory_workspace.restype = sz
+    lib.fovea_build_memory_workspace.argtypes = [vp, i64]
     lib.fovea_build_memory.restype = ctypes.c_int
-    lib.fovea_build_memory.argtypes = [vp, i64, vp, vp, vp, vp]
+    lib.fovea_build_memory.argtypes = [vp, i64, vp, vp, vp, vp, sz, vp]
     lib.fovea_retrieve_fuse_workspace.restype = sz
-    lib.fovea_retrieve_fuse_workspace.argtypes = [vp, i32, i32, i32]
+    lib.fovea_retrieve_fuse_workspace.argtypes = [vp, i32, i32, i64, i32, i32]
     lib.fovea_retrieve_fuse.restype = ctypes.c_int
     lib.fovea_retrieve_fuse.argtypes = [
         vp, i32, vp, i64, i32, vp, vp, vp, vp, i32, i32, vp, vp, vp, i32, i32,
@@ -178,15 +181,22 @@ def fovea_destroy(ctx: int) -> None:
     lib.fovea_destroy(ctx)
 
 
+def fovea_build_memory_workspace(ctx: int, n_rows: int) -> int:
+    return lib.fovea_build_memory_workspace(ctx, n_rows)
+
+
 def fovea_build_memory(ctx: int, V: torch.Tensor, keys: torch.Tensor, values: torch.Tensor,
-                       stream=None) -> None:
+                       workspace=None, stream=None) -> None:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.fovea_build_memory(ctx, V.shape[0], _ptr(V, None, "V"), _ptr(keys, V.dtype, "keys"),
-                                  _ptr(values, V.dtype, "values"), _stream(stream)),
+                                  _ptr(values, V.dtype, "values"), _ptr(workspace, None, "workspace"),
+                                  ws_bytes, _stream(stream)),
            "fovea_build_memory")
 
 
-def fovea_retrieve_fuse_workspace(ctx: int, n_nodes_total: int, m_max: int, k_max: int) -> int:
-    return lib.fovea_retrieve_fuse_workspace(ctx, n_nodes_total, m_max, k_max)
+def fovea_retrieve_fuse_workspace(ctx: int, B: int, n_nodes_total: int, n_mem_total: int,
+                                  m_max: int, k_max: int) -> int:
+    return lib.fovea_retrieve_fuse_workspace(ctx, B, n_nodes_total, n_mem_total, m_max, k_max)
 
 
 def fovea_retrieve_fuse(ctx: int, B: int, mem_off, n_mem_total: int, m_max: int, keys, values,
@@ -339,16 +349,24 @@ class Fovea:
 
     __del__ = close
 
-    def ensure_workspace(self, n_nodes_total: int, m_max: int, k_max: int) -> torch.Tensor:
-        need = fovea_retrieve_fuse_workspace(self.ctx, n_nodes_total, m_max, k_max)
+    def ensure_workspace(self, B: int, n_nodes_total: int, n_mem_total: int, m_max: int,
+                         k_max: int) -> torch.Tensor:
+        need = fovea_retrieve_fuse_workspace(self.ctx, B, n_nodes_total, n_mem_total, m_max, k_max)
         if self.workspace is None or self.workspace.numel() < need:
             self.workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         return self.workspace
 
-    def build_memory(self, V: torch.Tensor, stream=None):
-        keys = torch.empty(V.shape[0], self.dims.d_m, dtype=V.dtype, device=V.device)
-        values = torch.empty_like(keys)
-        fovea_build_memory(self.ctx, V, keys, values, stream)
+    def build_memory(self, V: torch.Tensor, keys: torch.Tensor | None = None,
+                     values: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                     stream=None):
+        if keys is None:
+            keys = torch.empty(V.shape[0], self.dims.d_m, dtype=V.dtype, device=V.device)
+        if values is None:
+            values = torch.empty_like(keys)
+        if workspace is None:
+            need = fovea_build_memory_workspace(self.ctx, V.shape[0])
+            workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        fovea_build_memory(self.ctx, V, keys, values, workspace, stream)
         return keys, values
 
     def alloc_outputs(self, n: int, k_max: int, d: int, d_m: int) -> Outputs:
@@ -369,7 +387,7 @@ class Fovea:
         k_max = inp["k_max"]
         if out is None:
             out = self.alloc_outputs(n, k_max, self.dims.d, self.dims.d_m)
-        ws = self.ensure_workspace(n, inp["m_max"], k_max)
+        ws = self.ensure_workspace(inp["mem_off"].numel() - 1, n, inp["keys"].shape[0], inp["m_max"], k_max)
         fovea_retrieve_fuse(
             self.ctx, inp["mem_off"].numel() - 1, inp["mem_off"], inp["keys"].shape[0],
             inp["m_max"], inp["keys"], inp["values"], inp.get("valid"), inp["node_off"], n,

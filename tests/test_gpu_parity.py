@@ -246,7 +246,7 @@ def test_host_argument_errors(lib):
         fv.retrieve_fuse(dict(inp, k_max=2048))
     assert e.value.status == lib.FOVEA_ERR_UNSUPPORTED
     out = fv.alloc_outputs(case.n_nodes, case.k_max, wl.d, wl.d_m)
-    ws = fv.ensure_workspace(case.n_nodes, case.m_max, case.k_max)
+    ws = fv.ensure_workspace(case.workload.B, case.n_nodes, case.n_mem, case.m_max, case.k_max)
     with pytest.raises(lib.FoveaError) as e:   # workspace too small
         lib.fovea_retrieve_fuse(fv.ctx, 1, inp["mem_off"], case.n_mem, case.m_max, inp["keys"],
                                 inp["values"], None, inp["node_off"], case.n_nodes, case.t_max,
