@@ -174,6 +174,33 @@ fovea_status fovea_retrieve_fuse(fovea_ctx* ctx, int32_t B, const int64_t* mem_o
                                  float* r_out, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* Size of the device array behind fovea_retrieve_fuse_noalloc (one per GPU). */
+#define FOVEA_STATIC_WORKSPACE_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): fovea_retrieve_fuse with the same
+ * arguments and results, minus the workspace.  Its workspace is a fixed array of
+ * FOVEA_STATIC_WORKSPACE_BYTES in the library's device data, one per GPU, reserved when
+ * the library's code is loaded on that GPU and held until the process ends; its device
+ * address is read once per GPU by fovea_create.  This call allocates nothing, creates
+ * no events (the context's profiling and fovea_destroy's wait do not cover it: the
+ * caller synchronises its stream before fovea_destroy) and returns FOVEA_ERR_WORKSPACE
+ * when the sizes need more than the array holds (fovea_retrieve_fuse_workspace gives
+ * the need; e.g. 32 requests x 60 nodes with 576-entry memories at d = 4096, d_m = 1024
+ * need about 26 MB).  Every call on one GPU uses the same array, whose contents the
+ * previous call leaves behind (the call needs none of it): calls that overlap on one
+ * GPU (on different streams, or from different threads) race and must be serialised
+ * by the caller. */
+fovea_status fovea_retrieve_fuse_noalloc(fovea_ctx* ctx, int32_t B, const int64_t* mem_off,
+                                         int64_t n_mem_total, int32_t m_max, const void* keys,
+                                         const void* values, const uint8_t* valid,
+                                         const int32_t* node_off, int32_t n_nodes_total,
+                                         int32_t t_max, const void* h, const int32_t* depth,
+                                         const float* tau, int32_t k_min, int32_t k_max,
+                                         void* h_out, int32_t* k_out, int32_t* idx_out,
+                                         float* gate_out, float* mass_out, float* r_out,
+                                         hipStream_t stream);
+
 /* Sticky bit of fovea_retrieve_fuse_backward: a node's K or selected index is outside
  * [0, min(k_max, M_b)] / [0, M_b) (its gradients are skipped and its dh row is NaN). */
 #define FOVEA_DATA_BAD_SELECTION 0x10u

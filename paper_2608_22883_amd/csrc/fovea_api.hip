@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -45,6 +46,7 @@ struct fovea_ctx {
   float b_g2;
   float* rms_w;  // [d] or null
   uint32_t* err;  // sticky device-data error bits
+  void* scratch;  // device address of this device's no-allocation workspace
   size_t lds_limit[5];  // dynamic LDS limit of each LdsKernel
   // one completion event per stream that calls have enqueued work on: fovea_destroy
   // waits for these (not for the whole device) before it frees the packed weights
@@ -181,8 +183,9 @@ struct ProfScope {
   int slot;
   hipStream_t s;
   hipEvent_t e0 = nullptr;
+  // c_ == nullptr: no events (the no-allocation entry point creates none)
   ProfScope(fovea_ctx* c_, int slot_, hipStream_t s_) : c(c_), slot(slot_), s(s_) {
-    if (c->prof && (e0 = prof_event(c)) != nullptr) (void)hipEventRecord(e0, s);
+    if (c != nullptr && c->prof && (e0 = prof_event(c)) != nullptr) (void)hipEventRecord(e0, s);
   }
   ~ProfScope() {
     if (e0 == nullptr) return;
@@ -328,6 +331,7 @@ struct RFArgs {
   float* mass_out;
   float* r_out;
   char* ws;
+  bool track;  // profiling events and the per-stream completion event (false: create none)
 };
 
 // Keys per score block: 16 kb, kb in {1, 2, 4, 5, 6}, whichever spreads B * tiles blocks
@@ -400,6 +404,7 @@ int score_parts(const fovea_dims& D, int B, int n, int m_max, int t_max) {
 template <typename T>
 fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   const fovea_dims& D = c->dims;
+  fovea_ctx* const pc = a.track ? c : nullptr;  // profiling context, if any
   const WsLayout L = ws_layout(D, a.n, a.m_max);
   const SplitK ksp = forward_splitk(D, a.n);
   float* splitk = reinterpret_cast<float*>(a.ws + L.splitk);
@@ -418,7 +423,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
 
   // 1. LayerNorm statistics of h, node -> request map, depth / tau / offset checks
   {
-    ProfScope ps(c, kRowStats, s);
+    ProfScope ps(pc, kRowStats, s);
     hipLaunchKernelGGL(row_stats_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, h, D.d,
                        D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
                        a.mem_off, a.n_mem, a.m_max, node_req, info, c->err);
@@ -443,7 +448,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     epi.q = q;
     epi.P = P;
     const int ks = ksp.hq;
-    ProfScope ps(c, kHq, s);
+    ProfScope ps(pc, kHq, s);
     // at most 64 rows: the same single row of tiles in 64-row tiles (no clamped rows)
     hipLaunchKernelGGL((a.n <= 64 ? hq_kernel<T, 64> : hq_kernel<T>), dim3(tile_grid(tm), ks), dim3(C::NT), 0,
                        s, tm, a.n, h, D.d, static_cast<const T*>(c->W_hq), epi, ks, splitk);
@@ -454,7 +459,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   // 3. scores for every (node, key) of each request
   if (a.m_max > 0) {
     const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.d_m)));
-    ProfScope ps(c, kScore, s);
+    ProfScope ps(pc, kScore, s);
     if constexpr (std::is_same<T, bf16_t>::value) {
       const int kb = score_keys_per_block(a.B, a.m_max) / 16;
       const int tiles = (a.m_max + 16 * kb - 1) / (16 * kb);
@@ -498,7 +503,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   sa.mass_out = a.mass_out;
   sa.err = c->err;
   {
-    ProfScope ps(c, kSelect, s);
+    ProfScope ps(pc, kSelect, s);
     const int VEC = D.dtype == FOVEA_BF16 ? 8 : 4;
     const int nch = (D.d_m / VEC + 63) / 64;  // 16-byte chunks per lane per value row
     // one wave selects a node of at most 1024 entries (16 keys per lane); larger memories
@@ -554,7 +559,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     epi.b1 = c->b1;
     epi.w_g2 = c->w_g2;
     epi.a_c = a_c;
-    ProfScope ps(c, kCorr1, s);
+    ProfScope ps(pc, kCorr1, s);
     hipLaunchKernelGGL(corr1_kernel<T>, dim3(tile_grid(tm), ksp.c1), dim3(C::NT), 0, s, tm, rT, D.d_m,
                        static_cast<const T*>(c->W1r), epi, gate_part, ksp.c1, splitk);
     if (ksp.c1 > 1)
@@ -585,7 +590,7 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     // split-K with the RMSNorm: the slices' sum, the residual and the norm in one pass
     fused_rms = ksp.c2 > 1 && c->rms_w != nullptr && D.d <= kCorr2RmsMaxD;
     {
-      ProfScope ps(c, kCorr2, s);
+      ProfScope ps(pc, kCorr2, s);
       hipLaunchKernelGGL((a.n <= 64 ? corr2_kernel<T, 64> : corr2_kernel<T>), dim3(tile_grid(tm), ksp.c2),
                          dim3(C::NT), 0, s, tm, a_c, static_cast<const T*>(c->W_c2), epi, ca, ksp.c2,
                          splitk);
@@ -594,14 +599,14 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
                            epi, ca, ksp.c2, static_cast<const float*>(splitk));
     }
     if (fused_rms) {
-      ProfScope ps(c, kRms, s);
+      ProfScope ps(pc, kRms, s);
       hipLaunchKernelGGL(corr2_rms_kernel<T>, dim3(a.n), dim3(256), 0, s, epi, ca, ksp.c2,
                          static_cast<const float*>(splitk), c->rms_w, D.rms_eps);
     }
   }
   // 7. RMSNorm
   if (c->rms_w && !fused_rms) {
-    ProfScope ps(c, kRms, s);
+    ProfScope ps(pc, kRms, s);
     hipLaunchKernelGGL(rms_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, D.d, rms_part, c->rms_w,
                        D.rms_eps, h_out);
   }
@@ -1150,6 +1155,39 @@ fovea_status run_mem_backward(fovea_ctx* c, const fovea_params* P, int n, const 
 
 }  // namespace
 
+// ---------------------------------------------------------------------------------
+// Workspace of the no-allocation entry point: one array in the code object's device
+// data (zero-initialised storage: no space in the library file), which each GPU the
+// library runs on holds until the process ends.  Host code never passes `scratch`
+// itself (on the host it is only a stand-in symbol): its device address on each GPU
+// is read once, with that GPU current, by hipGetSymbolAddress, and only that address
+// reaches kernels.  Every call on one GPU shares the array.
+// ---------------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[FOVEA_STATIC_WORKSPACE_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];
+
+// Device address of `scratch` on `device`, which must be the current device.
+fovea_status scratch_address(int device, void** out) {
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return FOVEA_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[device] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return FOVEA_ERR_DEVICE;
+    g_scratch_addr[device] = p;
+  }
+  *out = g_scratch_addr[device];
+  return FOVEA_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int fovea_abi_version(void) { return FOVEA_ABI_VERSION; }
@@ -1185,7 +1223,7 @@ fovea_status fovea_create(fovea_ctx** out, const fovea_dims* dims, const fovea_p
   c->bf16 = dims->dtype == FOVEA_BF16;
   c->es = c->bf16 ? 2 : 4;
   c->b_g2 = p->b_g2;
-  if (hipGetDevice(&c->device) != hipSuccess) {
+  if (hipGetDevice(&c->device) != hipSuccess || scratch_address(c->device, &c->scratch) != FOVEA_OK) {
     delete c;
     return FOVEA_ERR_DEVICE;
   }
@@ -1293,14 +1331,15 @@ size_t fovea_retrieve_fuse_workspace(const fovea_ctx* c, int32_t B, int32_t n_no
   return ws_layout(c->dims, n_nodes_total, m_max).total;
 }
 
-fovea_status fovea_retrieve_fuse(fovea_ctx* c, int32_t B, const int64_t* mem_off,
+static fovea_status retrieve_fuse_checked(fovea_ctx* c, int32_t B, const int64_t* mem_off,
                                  int64_t n_mem_total, int32_t m_max, const void* keys,
                                  const void* values, const uint8_t* valid,
                                  const int32_t* node_off, int32_t n_nodes_total, int32_t t_max,
                                  const void* h, const int32_t* depth, const float* tau,
                                  int32_t k_min, int32_t k_max, void* h_out, int32_t* k_out,
                                  int32_t* idx_out, float* gate_out, float* mass_out, float* r_out,
-                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 bool track) {
   if (c == nullptr) return FOVEA_ERR_INVALID_ARG;
   if (B < 0 || n_mem_total < 0 || m_max < 0 || n_nodes_total < 0 || t_max < 0) return FOVEA_ERR_INVALID_ARG;
   if (k_max < 1 || k_min < 0 || k_min > k_max) return FOVEA_ERR_INVALID_ARG;
@@ -1350,8 +1389,43 @@ fovea_status fovea_retrieve_fuse(fovea_ctx* c, int32_t B, const int64_t* mem_off
   a.mass_out = mass_out;
   a.r_out = r_out;
   a.ws = static_cast<char*>(workspace);
+  a.track = track;
   const fovea_status st = c->bf16 ? run_retrieve_fuse<bf16_t>(c, a, stream) : run_retrieve_fuse<float>(c, a, stream);
-  return st == FOVEA_OK ? record_use(c, stream) : st;
+  return st == FOVEA_OK && track ? record_use(c, stream) : st;
+}
+
+fovea_status fovea_retrieve_fuse(fovea_ctx* c, int32_t B, const int64_t* mem_off,
+                                 int64_t n_mem_total, int32_t m_max, const void* keys,
+                                 const void* values, const uint8_t* valid,
+                                 const int32_t* node_off, int32_t n_nodes_total, int32_t t_max,
+                                 const void* h, const int32_t* depth, const float* tau,
+                                 int32_t k_min, int32_t k_max, void* h_out, int32_t* k_out,
+                                 int32_t* idx_out, float* gate_out, float* mass_out, float* r_out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return retrieve_fuse_checked(c, B, mem_off, n_mem_total, m_max, keys, values, valid, node_off,
+                               n_nodes_total, t_max, h, depth, tau, k_min, k_max, h_out, k_out,
+                               idx_out, gate_out, mass_out, r_out, workspace, workspace_bytes,
+                               stream, true);
+}
+
+fovea_status fovea_retrieve_fuse_noalloc(fovea_ctx* c, int32_t B, const int64_t* mem_off,
+                                         int64_t n_mem_total, int32_t m_max, const void* keys,
+                                         const void* values, const uint8_t* valid,
+                                         const int32_t* node_off, int32_t n_nodes_total,
+                                         int32_t t_max, const void* h, const int32_t* depth,
+                                         const float* tau, int32_t k_min, int32_t k_max,
+                                         void* h_out, int32_t* k_out, int32_t* idx_out,
+                                         float* gate_out, float* mass_out, float* r_out,
+                                         hipStream_t stream) {
+  if (c == nullptr) return FOVEA_ERR_INVALID_ARG;
+  if (c->scratch == nullptr) return FOVEA_ERR_DEVICE;
+  if (B >= 0 && n_nodes_total >= 0 && n_mem_total >= 0 && m_max >= 0 && k_max >= 1 &&
+      ws_layout(c->dims, n_nodes_total, m_max).total > FOVEA_STATIC_WORKSPACE_BYTES)
+    return FOVEA_ERR_WORKSPACE;
+  return retrieve_fuse_checked(c, B, mem_off, n_mem_total, m_max, keys, values, valid, node_off,
+                               n_nodes_total, t_max, h, depth, tau, k_min, k_max, h_out, k_out,
+                               idx_out, gate_out, mass_out, r_out, c->scratch,
+                               FOVEA_STATIC_WORKSPACE_BYTES, stream, false);
 }
 
 fovea_status fovea_last_error(fovea_ctx* c, hipStream_t stream, uint32_t* bits) {

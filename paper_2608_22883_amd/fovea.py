@@ -40,7 +40,7 @@ FOVEA_LM_MAX_ROWS = 1 << 20
 EXPORTED = [
     "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
     "fovea_build_memory_workspace", "fovea_build_memory", "fovea_retrieve_fuse_workspace",
-    "fovea_retrieve_fuse",
+    "fovea_retrieve_fuse", "fovea_retrieve_fuse_noalloc",
     "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
     "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward",
     "fovea_build_memory_backward_workspace", "fovea_build_memory_backward",
@@ -99,6 +99,10 @@ def _load() -> ctypes.CDLL:
     lib.fovea_retrieve_fuse.argtypes = [
         vp, i32, vp, i64, i32, vp, vp, vp, vp, i32, i32, vp, vp, vp, i32, i32,
         vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.fovea_retrieve_fuse_noalloc.restype = ctypes.c_int
+    lib.fovea_retrieve_fuse_noalloc.argtypes = [
+        vp, i32, vp, i64, i32, vp, vp, vp, vp, i32, i32, vp, vp, vp, i32, i32,
+        vp, vp, vp, vp, vp, vp, vp]
     lib.fovea_last_error.restype = ctypes.c_int
     lib.fovea_last_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.fovea_profile.restype = ctypes.c_int
@@ -216,6 +220,26 @@ def fovea_retrieve_fuse(ctx: int, B: int, mem_off, n_mem_total: int, m_max: int,
         _ptr(r_out, torch.float32, "r_out"), _ptr(workspace, None, "workspace"), ws_bytes,
         _stream(stream))
     _check(st, "fovea_retrieve_fuse")
+
+
+FOVEA_STATIC_WORKSPACE_BYTES = 64 << 20
+
+
+def fovea_retrieve_fuse_noalloc(ctx: int, B: int, mem_off, n_mem_total: int, m_max: int, keys,
+                                values, valid, node_off, n_nodes_total: int, t_max: int, h, depth,
+                                tau, k_min: int, k_max: int, h_out, k_out=None, idx_out=None,
+                                gate_out=None, mass_out=None, r_out=None, stream=None) -> None:
+    """fovea_retrieve_fuse on the library's fixed per-GPU workspace (no allocation)."""
+    st = lib.fovea_retrieve_fuse_noalloc(
+        ctx, B, _ptr(mem_off, torch.int64, "mem_off"), n_mem_total, m_max,
+        _ptr(keys, h.dtype, "keys"), _ptr(values, h.dtype, "values"),
+        _ptr(valid, torch.uint8, "valid"), _ptr(node_off, torch.int32, "node_off"),
+        n_nodes_total, t_max, _ptr(h, None, "h"), _ptr(depth, torch.int32, "depth"),
+        _ptr(tau, torch.float32, "tau"), k_min, k_max, _ptr(h_out, h.dtype, "h_out"),
+        _ptr(k_out, torch.int32, "k_out"), _ptr(idx_out, torch.int32, "idx_out"),
+        _ptr(gate_out, torch.float32, "gate_out"), _ptr(mass_out, torch.float32, "mass_out"),
+        _ptr(r_out, torch.float32, "r_out"), _stream(stream))
+    _check(st, "fovea_retrieve_fuse_noalloc")
 
 
 def fovea_lm_topk_workspace(ctx: int, n_rows: int, vocab: int, k: int) -> int:

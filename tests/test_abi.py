@@ -28,7 +28,7 @@ def test_header_declares_the_entry_points():
     assert _declared() == sorted([
         "fovea_abi_version", "fovea_status_str", "fovea_create", "fovea_destroy",
         "fovea_build_memory_workspace", "fovea_build_memory", "fovea_retrieve_fuse_workspace",
-        "fovea_retrieve_fuse",
+        "fovea_retrieve_fuse", "fovea_retrieve_fuse_noalloc",
         "fovea_last_error", "fovea_profile", "fovea_profile_read", "fovea_lm_topk_workspace",
         "fovea_lm_topk", "fovea_retrieve_fuse_backward_workspace", "fovea_retrieve_fuse_backward",
         "fovea_build_memory_backward_workspace", "fovea_build_memory_backward"])
@@ -95,6 +95,9 @@ def test_null_context_paths(lib):
                                      None, None, 0, 1, None, None, None, None, None, None, None,
                                      0, None)
     assert st == lib.FOVEA_ERR_INVALID_ARG
+    st = lib.lib.fovea_retrieve_fuse_noalloc(None, 1, None, 0, 0, None, None, None, None, 0, 0, None,
+                                             None, None, 0, 1, None, None, None, None, None, None, None)
+    assert st == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_build_memory(None, 1, None, None, None, None, 0, None) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_last_error(None, None, None) == lib.FOVEA_ERR_INVALID_ARG
     assert lib.lib.fovea_profile(None, 1) == lib.FOVEA_ERR_INVALID_ARG
@@ -115,7 +118,7 @@ def test_null_context_paths(lib):
 def test_header_limits_match_the_binding(lib):
     src = open(HEADER).read()
     for name in ("FOVEA_MAX_M", "FOVEA_MAX_KMAX", "FOVEA_LM_MAX_K", "FOVEA_LM_MAX_VOCAB",
-                 "FOVEA_LM_MAX_ROWS"):
+                 "FOVEA_LM_MAX_ROWS", "FOVEA_STATIC_WORKSPACE_BYTES"):
         m = re.search(r"#define\s+" + name + r"\s+\(?([0-9]+)u?(?:\s*<<\s*([0-9]+))?", src)
         assert m, name
         val = int(m.group(1)) << int(m.group(2) or 0)
