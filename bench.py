@@ -137,7 +137,7 @@ def kernel_model(wl, case, union_rows, k_sum, lm=None, kc=0):
         k["lm_merge"] = dict(bytes=cand + n * kc * 8, flops=0)
     # the retrieval as one operation: every key, q, the selected value rows, r
     retrieval = dict(bytes=n_mem * d_m * es + n * d_m * 4 + union_rows * d_m * es + n * d_m * es,
-                     flops=2 * pairs * d_m)
+                     flops=2 * pairs * d_m + 2 * int(k_sum) * d_m)
     return k, retrieval
 
 
@@ -347,6 +347,20 @@ def main():
     ms = e0.elapsed_time(e1) / args.steps
     log(f"[bench] {args.steps} steps: {ms * 1e3:.1f} us/step")
 
+    # distribution of single-step times (events around every step, a separate pass so
+    # that the timed region above holds nothing but the steps)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for i in range(args.steps):
+        evs[i][0].record()
+        step(i)
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    pct = dict(p10=round(float(np.percentile(per, 10)), 2), median=round(float(np.median(per)), 2),
+               p90=round(float(np.percentile(per, 90)), 2), mean=round(float(per.mean()), 2))
+    log(f"[bench] single steps: p10 {pct['p10']} us, median {pct['median']} us, p90 {pct['p90']} us")
+
     # per-kernel timing (events around each kernel, on the library's stream)
     fovea_profile(fv.ctx, True)
     for i in range(args.steps):
@@ -381,7 +395,8 @@ def main():
     else:
         roof = dict(bound="hbm", achieved=dom["GBs"], peak=PEAK_HBM_GBS, unit="GB/s",
                     frac=dom["frac"], traffic=measured_traffic(dom["name"]), kernel=dom["name"])
-    ret_us = sum(k["avg_us"] for k in kernels if k["name"] in ("score", "select_gather"))
+    ret_names = [k["name"] for k in kernels if k["name"] in ("score", "select_gather")]
+    ret_us = sum(k["avg_us"] for k in kernels if k["name"] in ret_names)
     ret_gbs = retrieval["bytes"] / (ret_us * 1e-6) / 1e9 if ret_us else 0.0
 
     metric = "draft states/sec for retrieve+fuse (M=576, d=4096); % of peak HBM GB/s"
@@ -400,7 +415,8 @@ def main():
                     **({} if lm is None else dict(lm_head=lm["name"], vocab=lm["vocab"],
                                                   kc=args.kc))),
         roofline=roof,
-        retrieval=dict(kernels=["score", "select_gather"], us=round(ret_us, 2),
+        step_us=pct,
+        retrieval=dict(kernels=ret_names, us=round(ret_us, 2),
                        alg_bytes=retrieval["bytes"], GBs=round(ret_gbs, 1),
                        frac=round(ret_gbs / PEAK_HBM_GBS, 4)),
         kernels=kernels,
