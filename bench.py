@@ -40,7 +40,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0    # dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3     # dense fp32
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_batched_b32.txt")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def log(*a):
@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--kc", type=int, default=6, help="candidates per node with --lm-head")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the step (fp32) instead of the forward")
+    ap.add_argument("--build-memory", action="store_true",
+                    help="time the one-off memory build (every request's visual tokens -> keys "
+                         "and values) of the workload instead of the draft step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
     return ap.parse_args()
@@ -79,12 +82,13 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from the committed counter summary (FETCH_SIZE +
-    WRITE_SIZE, scaled by a plain copy's readings), or None when the summary is missing
-    or was taken on other sources."""
+def measured_traffic(kernel: str, run: str):
+    """HBM bytes per launch of `kernel` in run `run` (a workload name, with a suffix for
+    the other modes) from the committed counter summary profiles/traffic_<run>.txt
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's readings), or None when the
+    summary is missing or was taken on other sources."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(PROFILES, f"traffic_{run}.txt")) as f:
             rows = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
     except OSError:
         return None
@@ -236,7 +240,10 @@ def backward_main(args):
         per_step_us = tot / args.steps * 1e3
         e = dict(name=name, us_per_step=round(per_step_us, 2), timed_regions_per_step=cnt // args.steps)
         if name == "bwd_gemm":
+            # fp32-accurate products as bf16 GEMMs over a tripled K (hi/lo planes): the
+            # matrix cores issue three times the products' flops
             e["TFLOPs"] = round(gemm_flops / (per_step_us * 1e-6) / 1e12, 2)
+            e["MFMA_TFLOPs"] = round(3 * gemm_flops / (per_step_us * 1e-6) / 1e12, 2)
         kernels.append(e)
         log(f"[bench] {name:14s} {per_step_us:9.2f} us/step  ({cnt // args.steps} timed regions)")
     kernels.sort(key=lambda k: -k["us_per_step"])
@@ -248,10 +255,112 @@ def backward_main(args):
         vs_baseline=None, dtype="f32", data="synthetic",
         config=dict(workload=wl.name, mode="backward", B=wl.B, T=wl.T, M=wl.M, d=d, d_m=d_m,
                     d_c=d_c, k_max=wl.k_max, states_per_step=n),
-        roofline=dict(bound="mfma", achieved=gk["TFLOPs"], peak=PEAK_FP32_TFLOPS, unit="TFLOP/s",
-                      frac=round(gk["TFLOPs"] / PEAK_FP32_TFLOPS, 4), traffic=None,
-                      kernel="bwd_gemm (all GEMM launches of a step)"),
+        roofline=dict(bound="mfma", achieved=gk["MFMA_TFLOPs"], peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                      frac=round(gk["MFMA_TFLOPs"] / PEAK_BF16_TFLOPS, 4), traffic=None,
+                      kernel="bwd_gemm (all GEMM launches of a step; bf16 matrix cores, K tripled "
+                             "by the hi/lo planes of the fp32 operands)"),
         kernels=kernels)
+    fv.close()
+    print(json.dumps(line), flush=True)
+
+
+def build_main(args):
+    """One step = one fovea_build_memory call over every request's visual tokens (the
+    workload's B memories of M rows: LayerNorm over d_v, then W_K and W_U)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2608_22883_amd as F
+    from synth import WORKLOADS, make_memory_case
+
+    wl = WORKLOADS[args.workload]
+    n_rows = wl.B * wl.M
+    log(f"[bench] generating {n_rows} visual tokens of width {wl.d} ...")
+    V, W = make_memory_case(wl, n_rows)
+    dev = torch.device("cuda:0")
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    dims = dict(d=wl.d, d_v=wl.d, d_m=wl.d_m, d_c=wl.d_c, n_depth=wl.n_depth,
+                dtype=1 if wl.dtype == "bf16" else 0, ln_eps=W["ln_eps"], rms_eps=W["rms_eps"])
+    fv = F.Fovea(dims, W, device=dev)
+    Vd = torch.tensor(V, dtype=dt, device=dev)
+    # copies at distinct addresses so that consecutive calls cannot hit in the 256 MB MALL
+    sets = [Vd] + [Vd.clone() for _ in range(args.copies - 1)]
+    keys = torch.empty(n_rows, wl.d_m, dtype=dt, device=dev)
+    values = torch.empty_like(keys)
+    ws = torch.empty(max(F.fovea_build_memory_workspace(fv.ctx, n_rows), 256), dtype=torch.uint8,
+                     device=dev)
+
+    def step(i):
+        F.fovea_build_memory(fv.ctx, sets[i % len(sets)], keys, values, ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"[bench] build_memory, {args.steps} calls: {ms * 1e3:.1f} us/call")
+    F.fovea_profile(fv.ctx, True)
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    prof = F.fovea_profile_read(fv.ctx)
+    F.fovea_profile(fv.ctx, False)
+    es = 2 if wl.dtype == "bf16" else 4
+    d_v, d_m = wl.d, wl.d_m
+    model = dict(mem_row_stats=dict(bytes=n_rows * d_v * es + n_rows * 8, flops=3 * n_rows * d_v),
+                 mem_proj=dict(bytes=n_rows * d_v * es + 2 * d_m * d_v * es + 2 * n_rows * d_m * es,
+                               flops=2 * n_rows * d_v * 2 * d_m))
+    peak_fl = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    kernels = []
+    for name, (tot, cnt) in prof.items():
+        avg_ms = tot / cnt
+        m = model.get(name, dict(bytes=0, flops=0))
+        gbs = m["bytes"] / (avg_ms * 1e-3) / 1e9
+        tfl = m["flops"] / (avg_ms * 1e-3) / 1e12
+        mfma = name == "mem_proj"
+        kernels.append(dict(name=name, avg_us=round(avg_ms * 1e3, 2), launches=cnt,
+                            alg_bytes=m["bytes"], alg_flops=m["flops"], GBs=round(gbs, 1),
+                            TFLOPs=round(tfl, 2), bound="mfma" if mfma else "hbm",
+                            frac=round(tfl / peak_fl if mfma else gbs / PEAK_HBM_GBS, 4)))
+        log(f"[bench] {name:14s} {avg_ms * 1e3:8.2f} us  {gbs:8.1f} GB/s  {tfl:7.2f} TFLOP/s")
+    kernels.sort(key=lambda k: -k["avg_us"])
+    pk = next(k for k in kernels if k["name"] == "mem_proj")
+    line = dict(
+        metric="visual-memory rows/sec for build_memory (LayerNorm, W_K and W_U)",
+        value=round(n_rows / (ms * 1e-3), 1), unit="rows/s", n_gpus=1, steps=args.steps,
+        warmup=args.warmup, ms_per_step=round(ms, 5), higher_is_better=True, scaling="weak",
+        vs_baseline=None, dtype=wl.dtype, data="synthetic",
+        config=dict(workload=wl.name, mode="build_memory", rows=n_rows, images=wl.B,
+                    rows_per_image=wl.M, d_v=d_v, d_m=d_m, input_copies=len(sets)),
+        roofline=dict(bound="mfma", achieved=pk["TFLOPs"], peak=peak_fl, unit="TFLOP/s",
+                      frac=pk["frac"], traffic=measured_traffic("mem_proj", wl.name + "_build"),
+                      kernel="mem_proj"),
+        kernels=kernels)
+    if not args.no_cpu_baseline:
+        # the oracle on whole images (M rows each) within the time budget
+        from threadpoolctl import threadpool_info
+
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            r0 = (reps % wl.B) * wl.M
+            oracle.build_memory(V[r0:r0 + wl.M], W["mem_ln_g"], W["mem_ln_b"], W["W_K"], W["W_U"],
+                                W["ln_eps"], gain_rounding="bf16" if wl.dtype == "bf16" else None)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds or el / reps * (reps + 1) > 2.5 * args.cpu_seconds:
+                break
+        line["cpu_baseline"] = dict(
+            value=reps * wl.M / el, unit="rows/s", cores=int(threads), kind="oracle",
+            sample=f"{reps} image(s) of {wl.M} rows, {el:.1f} s wall, fp64 NumPy, BLAS threads={threads}")
     fv.close()
     print(json.dumps(line), flush=True)
 
@@ -270,6 +379,9 @@ def main():
 
     if args.backward:
         backward_main(args)
+        return
+    if args.build_memory:
+        build_main(args)
         return
 
     import numpy as np
@@ -387,14 +499,15 @@ def main():
         log(f"[bench] {name:14s} {avg_ms * 1e3:8.2f} us  {gbs:8.1f} GB/s  {tfl:7.2f} TFLOP/s")
     kernels.sort(key=lambda k: -k["avg_us"])
     dom = kernels[0]
+    run = wl.name if lm is None else f"{wl.name}_{lm['name']}"
     if dom["bound"] == "mfma":
         roof = dict(bound="mfma", achieved=dom["TFLOPs"],
                     peak=PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS,
-                    unit="TFLOP/s", frac=dom["frac"], traffic=measured_traffic(dom["name"]),
+                    unit="TFLOP/s", frac=dom["frac"], traffic=measured_traffic(dom["name"], run),
                     kernel=dom["name"])
     else:
         roof = dict(bound="hbm", achieved=dom["GBs"], peak=PEAK_HBM_GBS, unit="GB/s",
-                    frac=dom["frac"], traffic=measured_traffic(dom["name"]), kernel=dom["name"])
+                    frac=dom["frac"], traffic=measured_traffic(dom["name"], run), kernel=dom["name"])
     ret_names = [k["name"] for k in kernels if k["name"] in ("score", "select_gather")]
     ret_us = sum(k["avg_us"] for k in kernels if k["name"] in ret_names)
     ret_gbs = retrieval["bytes"] / (ret_us * 1e-6) / 1e9 if ret_us else 0.0
