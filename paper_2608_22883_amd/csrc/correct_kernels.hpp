@@ -12,8 +12,10 @@ template <typename T>
 using Corr1Cfg = GemmCfg<T, 64, 4>;
 template <typename T, int BM = 128>
 using Corr2Cfg = GemmCfg<T, BM, 2>;
-template <typename T>
-using MemCfg = GemmCfg<T, 128, 4>;
+// memory build: 256-row tiles (three 48 KB stages, two thirds of a 128-row tile's operand
+// bytes per multiply-add) for bf16 memories of many rows, else 128-row tiles
+template <typename T, int BM = 128>
+using MemCfg = GemmCfg<T, BM, BM == 256 ? 3 : 4>;
 constexpr int kPartCols = 128;  // columns reduced into one partial sum (one block tile)
 
 __host__ __device__ constexpr int n_parts(int cols) { return (cols + kPartCols - 1) / kPartCols; }
@@ -273,14 +275,14 @@ __global__ __launch_bounds__(256) void rms_kernel(int n, int d, const float* __r
 
 // Memory build: [keys | values] = LN(V) [W_K ; W_U]^T with the LayerNorm folded into the
 // epilogue exactly as in the query projection (c1 = W' 1, c2 = W b).
-template <typename T>
+template <typename T, int BM = 128>
 __global__ __launch_bounds__(256) void mem_proj_kernel(TileMap tm, int n, const T* __restrict__ V,
                                                        int d_v, const T* __restrict__ Wku, int d_m,
                                                        const float2* __restrict__ stats,
                                                        const float* __restrict__ c1,
                                                        const float* __restrict__ c2,
                                                        T* __restrict__ keys, T* __restrict__ values) {
-  using C = MemCfg<T>;
+  using C = MemCfg<T, BM>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
   if (!tm.map(tr, tc)) return;

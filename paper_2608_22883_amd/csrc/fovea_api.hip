@@ -295,15 +295,18 @@ fovea_status run_build(fovea_ctx* c, int n, const void* V, void* keys, void* val
                        static_cast<const int64_t*>(nullptr), int64_t{0}, 0,
                        static_cast<int32_t*>(nullptr), static_cast<NodeInfo*>(nullptr), c->err);
   }
-  using C = MemCfg<T>;
-  const TileMap tm = make_tile_map((n + C::BM - 1) / C::BM, (2 * D.d_m + C::BN - 1) / C::BN,
+  // 256-row tiles once the grid still holds at least 256 of them (bf16 only)
+  const bool tall = std::is_same<T, bf16_t>::value &&
+                    static_cast<int64_t>((n + 255) / 256) * ((2 * D.d_m + 127) / 128) >= 256;
+  const int BMv = tall ? 256 : 128;
+  const TileMap tm = make_tile_map((n + BMv - 1) / BMv, (2 * D.d_m + 127) / 128,
                                    static_cast<double>(n) * D.d_v, 2.0 * D.d_m * D.d_v);
   {
     ProfScope ps(c, kMemProj, s);
-    hipLaunchKernelGGL(mem_proj_kernel<T>, dim3(tile_grid(tm)), dim3(C::NT), 0, s, tm, n,
-                       static_cast<const T*>(V), D.d_v, static_cast<const T*>(c->W_KU), D.d_m,
-                       build_stats, c->m_c1, c->m_c2, static_cast<T*>(keys),
-                       static_cast<T*>(values));
+    hipLaunchKernelGGL((tall ? mem_proj_kernel<T, 256> : mem_proj_kernel<T, 128>), dim3(tile_grid(tm)),
+                       dim3(256), 0, s, tm, n, static_cast<const T*>(V), D.d_v,
+                       static_cast<const T*>(c->W_KU), D.d_m, build_stats, c->m_c1, c->m_c2,
+                       static_cast<T*>(keys), static_cast<T*>(values));
   }
   FOVEA_HIP(hipGetLastError());
   return FOVEA_OK;

@@ -173,10 +173,12 @@ def test_masked_and_ragged_and_empty(lib, dtype):
         assert case.valid[case.mem_off[b] + sel].all()
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_build_memory(lib, dtype):
+@pytest.mark.parametrize("dtype,rows", [("f32", 333), ("bf16", 333), ("bf16", 16400)])
+def test_build_memory(lib, dtype, rows):
+    # 333 rows: 128-row tiles; 16400 bf16 rows with d_m = 256: 65 x 4 tiles of 256 rows, the last
+    # row tile ragged
     wl = _small(dtype)
-    V, W = make_memory_case(wl, 333, affine="random")
+    V, W = make_memory_case(wl, rows, affine="random")
     import oracle
     fv = _ctx(lib, wl, W)
     dt = torch.bfloat16 if dtype == "bf16" else torch.float32
