@@ -100,7 +100,11 @@ SplitK forward_splitk(const fovea_dims& D, int64_t n) {
   const int bk = D.dtype == FOVEA_BF16 ? 64 : 32;
   const int ni = static_cast<int>(n);
   SplitK k;
-  k.hq = splitk_slices(((ni + 127) / 128) * ((D.d_m + 2 * D.d_c + 127) / 128), D.d, bk);
+  // at most 8 slices (one request: 16 slices of 256 columns 56.0 -> 8 of 512 53.8 us per
+  // step, the combine reading half the partials); the combine merges the slices' LayerNorm
+  // statistics in registers (at most kHqMaxKs)
+  static_assert(kHqMaxKs >= 8, "query GEMM slices");
+  k.hq = std::min(splitk_slices(((ni + 127) / 128) * ((D.d_m + 2 * D.d_c + 127) / 128), D.d, bk), 8);
   k.c1 = splitk_slices(((ni + 63) / 64) * ((2 * D.d_c + 127) / 128), D.d_m, bk);
   k.c2 = splitk_slices(((ni + 127) / 128) * ((D.d + 127) / 128), D.d_c, bk);
   return k;
@@ -112,7 +116,9 @@ WsLayout ws_layout(const fovea_dims& dm, int64_t n, int64_t m_max) {
   size_t o = 0;
   L.node_req = o; o = align_up(o + n * 4);
   L.info = o; o = align_up(o + n * sizeof(NodeInfo));
-  L.stats = o; o = align_up(o + n * 8);
+  // LayerNorm statistics: (mean, rstd) per node, or with a split-K query GEMM the
+  // slices' (mean, M2) per node
+  L.stats = o; o = align_up(o + std::max(1, forward_splitk(dm, n).hq) * n * 8);
   L.q = o; o = align_up(o + n * dm.d_m * (dm.dtype == FOVEA_BF16 ? 2 * kQSplitBf16 : 4));
   L.P = o; o = align_up(o + n * 2 * dm.d_c * 4);
   // scores; small bf16 batches may hold k-sliced partial scores (score_parts)
@@ -424,8 +430,10 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
   float* rms_part = reinterpret_cast<float*>(a.ws + L.rms_part);
   const T* h = static_cast<const T*>(a.h);
 
-  // 1. LayerNorm statistics of h, node -> request map, depth / tau / offset checks
-  {
+  // 1. LayerNorm statistics of h, node -> request map, depth / tau / offset checks (with
+  // a split-K query GEMM its slices and its combine do this, without a launch of its own)
+  const bool split_stats = ksp.hq > 1;
+  if (!split_stats) {
     ProfScope ps(pc, kRowStats, s);
     hipLaunchKernelGGL(row_stats_kernel<T>, dim3((a.n + 3) / 4), dim3(256), 0, s, a.n, h, D.d,
                        D.ln_eps, stats, a.depth, D.n_depth, a.node_off, a.B, a.t_max, a.tau,
@@ -453,11 +461,30 @@ fovea_status run_retrieve_fuse(fovea_ctx* c, const RFArgs& a, hipStream_t s) {
     const int ks = ksp.hq;
     ProfScope ps(pc, kHq, s);
     // at most 64 rows: the same single row of tiles in 64-row tiles (no clamped rows)
-    hipLaunchKernelGGL((a.n <= 64 ? hq_kernel<T, 64> : hq_kernel<T>), dim3(tile_grid(tm), ks), dim3(C::NT), 0,
-                       s, tm, a.n, h, D.d, static_cast<const T*>(c->W_hq), epi, ks, splitk);
+    float2* stat_part = split_stats ? stats : nullptr;
+    NodeMapArgs nm;
+    {
+      nm.node_off = a.node_off;
+      nm.B = a.B;
+      nm.t_max = a.t_max;
+      nm.n = a.n;
+      nm.depth = a.depth;
+      nm.n_depth = D.n_depth;
+      nm.tau = a.tau;
+      nm.mem_off = a.mem_off;
+      nm.n_mem = a.n_mem;
+      nm.m_max = a.m_max;
+      nm.node_req = node_req;
+      nm.info = info;
+      nm.err = c->err;
+    }
+    hipLaunchKernelGGL((a.n <= 64 ? hq_kernel<T, 64> : hq_kernel<T>), dim3(tile_grid(tm), ks),
+                       dim3(C::NT), 0, s, tm, a.n, h, D.d, static_cast<const T*>(c->W_hq), epi, ks, splitk,
+                       stat_part, nm);
     if (ks > 1)
       hipLaunchKernelGGL(hq_combine_kernel<T>, dim3((N + 127) / 128, (a.n + 15) / 16), dim3(256), 0, s,
-                         epi, ks, static_cast<const float*>(splitk));
+                         epi, ks, static_cast<const float*>(splitk),
+                         static_cast<const float2*>(stat_part), D.d, D.ln_eps);
   }
   // 3. scores for every (node, key) of each request
   if (a.m_max > 0) {

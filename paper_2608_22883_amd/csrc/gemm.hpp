@@ -95,7 +95,7 @@ inline TileMap make_tile_map(int rb, int cb, double a_bytes, double b_bytes) {
   return m;
 }
 
-inline int tile_grid(const TileMap& m) {
+__host__ __device__ inline int tile_grid(const TileMap& m) {
   return 8 * ((m.rb + m.xr - 1) / m.xr) * ((m.cb + m.xc - 1) / m.xc);
 }
 

@@ -191,6 +191,92 @@ __global__ __launch_bounds__(256) void row_stats_kernel(int n, const T* __restri
   }
 }
 
+// Request of node `row` and its validation, by one thread (the same checks as the
+// statistics kernel): node_req[row] = b, or -1 for a node whose offsets, depth or tau are
+// bad; info[row] as in NodeInfo; the error bits are set.  Returns node_req[row] >= 0.
+struct NodeMapArgs {
+  const int32_t* node_off;
+  int B, t_max, n;
+  const int32_t* depth;
+  int n_depth;
+  const float* tau;
+  const int64_t* mem_off;
+  int64_t n_mem;
+  int m_max;
+  int32_t* node_req;
+  NodeInfo* info;
+  uint32_t* err;
+};
+
+__device__ __forceinline__ bool map_node(const NodeMapArgs& m, int row, bool write) {
+  int lo = 0, hi = m.B - 1;  // largest b with node_off[b] <= row (fixed step count)
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (m.node_off[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo;
+  const int t0 = m.node_off[b], t1 = m.node_off[b + 1], dep = m.depth[row];
+  const float tb = m.tau[b];
+  const int64_t m0 = m.mem_off[b], m1 = m.mem_off[b + 1];
+  uint32_t bad = 0;
+  if (!(0 <= t0 && t0 <= row && row < t1 && t1 <= m.n && t1 - t0 <= m.t_max)) bad |= kErrNodeOff;
+  if (dep < 0 || dep >= m.n_depth) bad |= kErrDepth;
+  if (!(tb >= 0.f && tb <= 1.f)) bad |= kErrTau;
+  const bool ok = bad == 0;
+  if (write) {
+    m.node_req[row] = ok ? b : -1;
+    const bool mem_ok = 0 <= m0 && m0 <= m1 && m1 <= m.n_mem && m1 - m0 <= m.m_max;
+    if (ok && !mem_ok) bad |= kErrMemOff;
+    NodeInfo ni;
+    ni.m0 = mem_ok ? m0 : 0;
+    ni.M = bad ? -1 : static_cast<int32_t>(m1 - m0);
+    ni.tau = tb;
+    m.info[row] = ni;
+    if (bad) atomicOr(m.err, bad);
+  }
+  return ok;
+}
+
+// LayerNorm statistics of the split-K query GEMM: the block of column tile tc over K slice
+// y (columns k0 .. k0 + Kc) writes, for the rows m0 + tc, m0 + tc + cb, .. of its row tile,
+// the slice's mean and sum of squared deviations from it (two passes over the slice,
+// which the GEMM has just brought into L2) to part[y][row]; the combine merges the slices.
+// The blocks of slice 0 also map and validate those rows (map_node).
+template <typename T>
+__device__ __forceinline__ void slice_row_stats(const T* __restrict__ h, int d, int n, int m0, int rows,
+                                                int tc, int cb, int k0, int Kc, int y,
+                                                float2* __restrict__ part, const NodeMapArgs& nm) {
+  // 8 consecutive elements per lane and step (Kc is a multiple of 64)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rend = min(m0 + rows, n);
+  for (int r = m0 + tc + cb * wave; r < rend; r += cb * 4) {
+    const T* hr = h + static_cast<int64_t>(r) * d + k0;
+    float s = 0.f;
+    for (int c = 8 * lane; c < Kc; c += 8 * 64) {
+      float x[8];
+      load8(hr + c, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += x[e];
+    }
+    const float mean = wave_sum_f32(s) / static_cast<float>(Kc);
+    float ss = 0.f;
+    for (int c = 8 * lane; c < Kc; c += 8 * 64) {
+      float x[8];
+      load8(hr + c, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float t = x[e] - mean;
+        ss = fmaf(t, t, ss);
+      }
+    }
+    const float m2 = wave_sum_f32(ss);
+    if (lane == 0) {
+      part[static_cast<int64_t>(y) * n + r] = make_float2(mean, m2);
+      if (y == 0) map_node(nm, r, true);  // the slice-0 blocks map and validate the rows
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------
 // Query projection with the LayerNorm folded into the epilogue:
 //   q = W_Q (LN(h) + E_dep[l]) = rstd * (W' h - mu * W' 1) + W_Q (b + E_dep[l]),
@@ -210,9 +296,11 @@ template <typename T>
 struct HqEpi {
   int n, d_m, N, n_depth;
   int64_t n_p;
-  const float2* stats;
+  const float2* stats;     // (mean, rstd) of row - srow0
   const int32_t* depth;
   const int32_t* node_req;
+  const int* ok_s = nullptr;  // if set: row - srow0 valid (else node_req[row] >= 0)
+  int srow0 = 0;
   const float* c1;
   const float* c2;
   T* q;
@@ -224,8 +312,8 @@ struct HqEpi {
       return 0.f;
     }
     const int64_t plane = static_cast<int64_t>(n) * d_m;
-    const float2 st = stats[row];
-    const bool ok = node_req[row] >= 0;
+    const float2 st = stats[row - srow0];
+    const bool ok = ok_s != nullptr ? ok_s[row - srow0] != 0 : node_req[row] >= 0;
     const int dep = min(max(depth[row], 0), n_depth - 1);
     float a[8], b[8], val[8];
     load8(c1 + col0, a);
@@ -251,10 +339,15 @@ struct HqEpi {
 
 // ks > 1: split-K (grid.y = ks slices, fp32 partials in part), finished by
 // hq_combine_kernel with the same epilogue.
+// With ks > 1 and stat_part set, the LayerNorm statistics come from the slices
+// (slice_row_stats, after each block's partial product) and the combine merges them;
+// no separate statistics launch.
 template <typename T, int BM = 128>
 __global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __restrict__ h, int d,
                                                  const T* __restrict__ Whq, HqEpi<T> epi, int ks,
-                                                 float* __restrict__ part) {
+                                                 float* __restrict__ part,
+                                                 float2* __restrict__ stat_part = nullptr,
+                                                 NodeMapArgs nm = NodeMapArgs{}) {
   using C = HqCfg<T, BM>;
   __shared__ __align__(16) unsigned char smem[C::SMEM_BYTES];
   int tr, tc;
@@ -262,6 +355,11 @@ __global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __r
   const int m0 = tr * C::BM, n0 = tc * C::BN;
   if (ks > 1) {
     gemm_splitk_partial<C>(h, d, n, Whq, d, epi.N, d, ks, m0, n0, part, smem);
+    if (stat_part != nullptr) {
+      const int Kc = d / ks;
+      slice_row_stats(h, d, n, m0, C::BM, tc, tm.cb, static_cast<int>(blockIdx.y) * Kc, Kc,
+                      static_cast<int>(blockIdx.y), stat_part, nm);
+    }
     return;
   }
   f32x4 acc[C::TM][C::TN];
@@ -269,10 +367,73 @@ __global__ __launch_bounds__(256) void hq_kernel(TileMap tm, int n, const T* __r
   gemm_epilogue<C>(acc, smem, m0, n0, epi, NoRowSum{});
 }
 
+// stat_part set: the block's 16 rows get their LayerNorm statistics by merging the ks
+// slices' (mean, M2) in slice order (Chan's pairwise update, equal slice widths) and their
+// validity from node_req (written by the slice-0 partial blocks).  Every thread first
+// adds its 8 columns' partials (as
+// splitk_combine does), so that those loads and the statistics' loads are in flight
+// together; then the barrier; then the epilogue.
+constexpr int kHqMaxKs = 32;  // the query GEMM's k slices are at most d / 128 <= 32 here
+
 template <typename T>
 __global__ __launch_bounds__(256) void hq_combine_kernel(HqEpi<T> epi, int ks,
-                                                         const float* __restrict__ part) {
-  splitk_combine(epi.n, epi.N, ks, part, epi, NoRowSum{});
+                                                         const float* __restrict__ part,
+                                                         const float2* __restrict__ stat_part,
+                                                         int d, float eps) {
+  if (stat_part == nullptr) {
+    splitk_combine(epi.n, epi.N, ks, part, epi, NoRowSum{});
+    return;
+  }
+  __shared__ float2 s_st[16];
+  __shared__ int s_ok[16];
+  const int r0 = static_cast<int>(blockIdx.y) * 16;
+  const int row = r0 + static_cast<int>(threadIdx.x >> 4);
+  const int col0 = static_cast<int>(blockIdx.x) * 128 + static_cast<int>(threadIdx.x & 15) * 8;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (row < epi.n && col0 < epi.N) {
+    for (int y0 = 0; y0 < ks; y0 += 8) {
+      float t[8][8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (y0 + u < ks) load8(part + (static_cast<int64_t>(y0 + u) * epi.n + row) * epi.N + col0, t[u]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (y0 + u < ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += t[u][e];
+    }
+  }
+  if (threadIdx.x < 16) {
+    const int srow = r0 + static_cast<int>(threadIdx.x);
+    float2 st = make_float2(0.f, 1.f);
+    int ok = 0;
+    if (srow < epi.n) {
+      float2 p[kHqMaxKs];
+#pragma unroll
+      for (int y = 0; y < kHqMaxKs; ++y)
+        if (y < ks) p[y] = stat_part[static_cast<int64_t>(y) * epi.n + srow];
+      ok = epi.node_req[srow] >= 0 ? 1 : 0;
+      const float w = static_cast<float>(d / ks);
+      float mean = 0.f, m2 = 0.f, cnt = 0.f;
+#pragma unroll
+      for (int y = 0; y < kHqMaxKs; ++y)
+        if (y < ks) {
+          const float c2 = cnt + w;
+          const float delta = p[y].x - mean;
+          mean += delta * (w / c2);
+          m2 += p[y].y + delta * delta * (cnt * w / c2);
+          cnt = c2;
+        }
+      st = make_float2(mean, 1.0f / sqrtf(m2 / static_cast<float>(d) + eps));
+    }
+    s_st[threadIdx.x] = st;
+    s_ok[threadIdx.x] = ok;
+  }
+  __syncthreads();
+  epi.stats = s_st;
+  epi.ok_s = s_ok;
+  epi.srow0 = r0;
+  epi(row, col0, v);  // rows and columns past the matrix are dropped by the functor
 }
 
 // ---------------------------------------------------------------------------------
