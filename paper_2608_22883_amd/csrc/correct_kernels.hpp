@@ -38,8 +38,13 @@ struct Corr1Epi {
   T* a_c;
   __device__ __forceinline__ float operator()(int row, int col0, const float (&v)[8]) const {
     if (row >= n || col0 >= N) return 0.f;
-    float p[8], b[8], pre[8];
+    float p[8];
     load8(P + static_cast<int64_t>(row) * N + col0, p);
+    return finish(row, col0, v, p);
+  }
+  // the epilogue for 8 columns whose P is given
+  __device__ __forceinline__ float finish(int row, int col0, const float (&v)[8], const float (&p)[8]) const {
+    float b[8], pre[8];
     load8(b1 + col0, b);
 #pragma unroll
     for (int e = 0; e < 8; ++e) pre[e] = v[e] + p[e] + b[e];
@@ -82,9 +87,30 @@ __global__ __launch_bounds__(256) void corr1_kernel(TileMap tm, const T* __restr
     gemm_splitk_partial<C>(rT, d_m, epi.n, W1r, d_m, epi.N, d_m, ks, m0, n0, part, smem);
     return;
   }
+  // each thread's P for the epilogue (8 fp32 per epilogue group, rows and columns clamped
+  // into the matrix) is loaded before the mainloop, so that its latency hides behind the
+  // matrix work
+  constexpr int PRE = C::WM * C::SROWS * 16 / C::NT;
+  f32x4 ppre[PRE][2];
+#pragma unroll
+  for (int gi = 0; gi < PRE; ++gi) {
+    int row, col0;
+    epilogue_group<C>(gi, m0, n0, row, col0);
+    const float* pp = epi.P + static_cast<int64_t>(min(row, epi.n - 1)) * epi.N + min(col0, epi.N - 8);
+    ppre[gi][0] = *reinterpret_cast<const f32x4*>(pp);
+    ppre[gi][1] = *reinterpret_cast<const f32x4*>(pp + 4);
+  }
   f32x4 acc[C::TM][C::TN];
   gemm_mainloop<C>(acc, rT, d_m, epi.n, W1r, d_m, epi.N, d_m, m0, n0, smem);
-  gemm_epilogue<C>(acc, smem, m0, n0, epi, RowPart{epi.n, n_parts(epi.N), tc, gate_part});
+  gemm_epilogue<C>(
+      acc, smem, m0, n0,
+      [&](int row, int col0, const float(&v)[8], int gi) -> float {
+        if (row >= epi.n || col0 >= epi.N) return 0.f;
+        const float p[8] = {ppre[gi][0][0], ppre[gi][0][1], ppre[gi][0][2], ppre[gi][0][3],
+                            ppre[gi][1][0], ppre[gi][1][1], ppre[gi][1][2], ppre[gi][1][3]};
+        return epi.finish(row, col0, v, p);
+      },
+      RowPart{epi.n, n_parts(epi.N), tc, gate_part});
 }
 
 template <typename T>

@@ -373,12 +373,28 @@ __device__ __forceinline__ void gemm_epilogue(const f32x4 (&acc)[C::TM][C::TN],
       const f32x4 hi = *reinterpret_cast<const f32x4*>(so + r * C::SLD + c8 * 8 + 4);
       const float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       const int row = m0 + p * C::SROWS + r;
-      float s = f(row, n0 + c8 * 8, v);
+      float s;
+      // functors that take the group index gi (compile-time after unrolling) can hold
+      // operands prefetched per group (epilogue_group)
+      if constexpr (std::is_invocable_v<F, int, int, const float(&)[8], int>)
+        s = f(row, n0 + c8 * 8, v, p * (GROUPS / C::NT) + g0 / C::NT);
+      else
+        s = f(row, n0 + c8 * 8, v);
       s = sum16(s);
       if ((lane & 15) == 0) fr(row, s);
     }
     __syncthreads();
   }
+}
+
+// Row and first column of epilogue group gi of this thread (gemm_epilogue's mapping):
+// groups per thread C::WM * C::SROWS * 16 / C::NT.
+template <class C>
+__device__ __forceinline__ void epilogue_group(int gi, int m0, int n0, int& row, int& col0) {
+  constexpr int PER = C::SROWS * 16 / C::NT;
+  const int p = gi / PER, g = (gi % PER) * C::NT + static_cast<int>(threadIdx.x);
+  row = m0 + p * C::SROWS + (g >> 4);
+  col0 = n0 + (g & 15) * 8;
 }
 
 struct NoRowSum {
