@@ -1251,6 +1251,21 @@ __device__ __forceinline__ void write_invalid_node(const SelectArgs<T>& a, int n
 
 __device__ __forceinline__ int ballot_count(bool p) { return __popcll(__ballot(p)); }
 
+// Number of lanes and slots j with key slot j >= t.  The NPL ballots are taken first
+// (each in its own scalar register pair) and counted afterwards, so that the compares
+// issue back to back instead of each waiting for the previous count to read the one
+// condition register.
+template <int NPL>
+__device__ __forceinline__ int count_ge(const uint32_t (&kv)[NPL], uint32_t t) {
+  unsigned long long b[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) b[j] = __builtin_amdgcn_ballot_w64(kv[j] >= t);
+  int c = 0;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) c += __popcll(b[j]);
+  return c;
+}
+
 __device__ __forceinline__ unsigned long long comp_key(uint32_t k, int i) {
   return (static_cast<unsigned long long>(k) << 32) |
          static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(i));
@@ -1374,9 +1389,7 @@ __device__ __forceinline__ int select_one_node(const SelectArgs<T>& a, int n, in
       }
       for (; bit >= 0; --bit) {
         const uint32_t t = thr | (1u << bit);
-        int cnt = 0;
-#pragma unroll
-        for (int j = 0; j < NPL; ++j) cnt += ballot_count(kv[j] >= t);
+        const int cnt = count_ge<NPL>(kv, t);
         if (cnt >= a.k_max) thr = t;
         if (cnt == a.k_max) break;
       }
