@@ -146,6 +146,26 @@ def test_cardinality_bounds(lib, dtype, k_min, k_max):
     assert (g["K"] <= k_max).all() and (g["K"] >= min(k_min, 300)).all()
 
 
+# The header's limits: request memories of FOVEA_MAX_M entries and k_max = FOVEA_MAX_KMAX
+# (block-wide selection, candidate sort past 256); the key scale puts K anywhere from a
+# few dozen entries to the full k_max.
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_maximum_sizes(lib, dtype):
+    max_m, max_k = lib.FOVEA_MAX_M, lib.FOVEA_MAX_KMAX
+    wl = WORKLOADS["llava_b1"].with_(dtype=dtype, d=512, d_m=256, B=2, T=6, M=max_m, k_min=0,
+                                     k_max=max_k, tau=0.3, tau_hi=0.95, key_scale=(20.0, 20.0))
+    case = make_case(wl, affine="random")
+    assert case.m_max == max_m
+    g, st, bits = _run(lib, case)
+    assert st == 0, f"data error bits {bits:#x}"
+    ref = run_oracle(case)
+    rep = {}
+    compare(case, g, ref, H_TOL[dtype], rep, label=f"maximum sizes {dtype}")
+    print(f"[gpu] maximum sizes {dtype}: K max {int(g['K'].max())} {rep}", flush=True)
+    assert rep["exempt"] <= rep["admissible"]
+    assert int(ref["K"].max()) == max_k and int(ref["K"].min()) < 256
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_masked_and_ragged_and_empty(lib, dtype):
     wl = _small(dtype, B=5, M=150, M_lo=1, T=6, valid_frac=0.6, tau=0.9)
