@@ -865,6 +865,10 @@ __device__ __forceinline__ RadixPick radix_pick(int* hist, int krem, RadixPick* 
   return *out;
 }
 
+// keys read per load round in the block-wide selection's scans over its LDS keys, for
+// memories of more than kSelScanB * 256 entries (shorter ones scan one key at a time)
+constexpr int kSelScanB = 8;
+
 // Dynamic LDS of select_gather_kernel: the order keys (or the gather's partial sums,
 // 3 x 64 lanes x VEC floats, whichever is larger; 8-byte aligned end), then the candidate
 // keys (8 B), prefix masses (8 B), weights (4 B) and indices (4 B) of kcap slots.
@@ -875,6 +879,14 @@ __host__ __device__ inline int select_key_bytes(int m_max, int vec) {
 }
 __host__ __device__ inline int select_gather_smem(int m_max, int k_max, int vec) {
   return select_key_bytes(m_max, vec) + select_kcap(k_max) * 24;
+}
+
+// exp(s - smax) of an order key as 2^((s - smax) log2 e) on the hardware exp2 (relative
+// error a few 1e-7, far inside the score rounding band); the normaliser, the prefix masses
+// and the weights all take it from here, so the prefixes never exceed the normaliser by a
+// differing rounding.
+__device__ __forceinline__ float key_mass(uint32_t k, float smax) {
+  return __builtin_amdgcn_exp2f((key_to_float(k) - smax) * 1.4426950408889634f);
 }
 
 // Sorts the C distinct keys of list descending in place: the rank of a key is the number
@@ -957,34 +969,42 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
   // keys, valid count, max
   int cnt = 0;
   uint32_t kmax = 0;
-  // four entries per thread and step, every load issued before the first use
-  for (int i0 = tid; i0 < M; i0 += 4 * NT) {
-    float sc[4], ps[4][kScoreMaxParts - 1];
-    bool v[4];
+  // U entries per thread and step, every load issued before the first use (16 for long
+  // memories, whose rows take many steps; 4 otherwise)
+  auto load_keys = [&](auto U_) {
+    constexpr int U = decltype(U_)::value;
+    for (int i0 = tid; i0 < M; i0 += U * NT) {
+      float sc[U], ps[U][kScoreMaxParts - 1];
+      bool v[U];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * NT;
-      const bool in = i < M;
-      sc[u] = in ? srow[i] : 0.f;
-#pragma unroll
-      for (int p = 1; p < kScoreMaxParts; ++p)
-        ps[u][p - 1] = in && p < a.s_parts ? srow[p * a.s_stride + i] : 0.f;
-      v[u] = in && (a.valid == nullptr || a.valid[m0 + i] != 0);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * NT;
-      if (i < M) {
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * NT;
+        const bool in = i < M;
+        sc[u] = in ? srow[i] : 0.f;
 #pragma unroll
         for (int p = 1; p < kScoreMaxParts; ++p)
-          if (p < a.s_parts) sc[u] += ps[u][p - 1];
-        const uint32_t k = v[u] ? order_key(sc[u]) : 0u;
-        skey[i] = k;
-        cnt += v[u] ? 1 : 0;
-        kmax = max(kmax, k);
+          ps[u][p - 1] = in && p < a.s_parts ? srow[p * a.s_stride + i] : 0.f;
+        v[u] = in && (a.valid == nullptr || a.valid[m0 + i] != 0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * NT;
+        if (i < M) {
+#pragma unroll
+          for (int p = 1; p < kScoreMaxParts; ++p)
+            if (p < a.s_parts) sc[u] += ps[u][p - 1];
+          const uint32_t k = v[u] ? order_key(sc[u]) : 0u;
+          skey[i] = k;
+          cnt += v[u] ? 1 : 0;
+          kmax = max(kmax, k);
+        }
       }
     }
-  }
+  };
+  if (M > 16 * NT)
+    load_keys(std::integral_constant<int, 16>());
+  else
+    load_keys(std::integral_constant<int, 4>());
   const int nV = block_sum_int<NT>(cnt, ired);
   kmax = block_max_u32<NT>(kmax, ured);
 
@@ -995,7 +1015,7 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
     double z = 0.0;
     for (int i = tid; i < M; i += NT) {
       const uint32_t k = skey[i];
-      if (k != 0u) z += static_cast<double>(expf(key_to_float(k) - smax));
+      if (k != 0u) z += static_cast<double>(key_mass(k, smax));
     }
     const double Z = block_sum_f64<NT>(z, dred);
 
@@ -1010,20 +1030,34 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
       for (int shift = 24; shift >= 0; shift -= 8) {
         hist[tid] = 0;
         __syncthreads();
-        // a thread's keys mostly share a digit: one atomic per run of equal digits
+        // a thread's keys mostly share a digit: one atomic per run of equal digits; the
+        // keys are read SB at a time (all reads issued before the first use)
         int cur = -1, run = 0;
-        for (int i = tid; i < M; i += NT) {
-          const uint32_t k = skey[i];
-          if (k != 0u && (k & pmask) == prefix) {
-            const int dg = static_cast<int>((k >> shift) & 255u);
-            if (dg != cur) {
-              if (run > 0) atomicAdd(&hist[cur], run);
-              cur = dg;
-              run = 0;
+        auto hist_scan = [&](auto SB_) {
+          constexpr int SB = decltype(SB_)::value;
+          for (int i0 = tid; i0 < M; i0 += SB * NT) {
+            uint32_t kk[SB];
+#pragma unroll
+            for (int u = 0; u < SB; ++u) kk[u] = i0 + u * NT < M ? skey[i0 + u * NT] : 0u;
+#pragma unroll
+            for (int u = 0; u < SB; ++u) {
+              const uint32_t k = kk[u];
+              if (k != 0u && (k & pmask) == prefix) {
+                const int dg = static_cast<int>((k >> shift) & 255u);
+                if (dg != cur) {
+                  if (run > 0) atomicAdd(&hist[cur], run);
+                  cur = dg;
+                  run = 0;
+                }
+                ++run;
+              }
             }
-            ++run;
           }
-        }
+        };
+        if (M > kSelScanB * NT)
+          hist_scan(std::integral_constant<int, kSelScanB>());
+        else
+          hist_scan(std::integral_constant<int, 1>());
         if (run > 0) atomicAdd(&hist[cur], run);
         __syncthreads();
         if (tid < 64) radix_pick(hist, krem, &pick);
@@ -1059,16 +1093,51 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
     }
     if (tid == 0) s_count = 0;
     __syncthreads();
-    for (int i = tid; i < M; i += NT) {
-      const uint32_t k = skey[i];
-      if (k == 0u) continue;
-      const bool take = nV <= a.k_max || k > thr ||
-                        (k == thr && (all_eq || 0xFFFFu - static_cast<uint32_t>(i) >= thr_inv));
-      if (take) {
-        const int pos = atomicAdd(&s_count, 1);
-        if (pos < kcap)
-          cand[pos] = (static_cast<unsigned long long>(k) << 32) |
-                      static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(i));
+    // the candidates appended in any order (the ranking below orders them); long memories:
+    // per wave one atomic per step for all its lanes' picks, keys read SB at a time
+    auto compact = [&](auto SB_) {
+      constexpr int SB = decltype(SB_)::value;
+      for (int i0 = tid - (tid & 63); i0 < M; i0 += SB * NT) {
+        uint32_t kk[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+          const int i = i0 + (tid & 63) + u * NT;
+          kk[u] = i < M ? skey[i] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+          const int i = i0 + (tid & 63) + u * NT;
+          const uint32_t k = kk[u];
+          const bool take = k != 0u && (nV <= a.k_max || k > thr ||
+                                        (k == thr && (all_eq || 0xFFFFu - static_cast<uint32_t>(i) >= thr_inv)));
+          const unsigned long long bal = __ballot(take);
+          if (bal == 0ull) continue;  // wave-uniform
+          int base = 0;
+          if ((tid & 63) == __ffsll(static_cast<long long>(bal)) - 1) base = atomicAdd(&s_count, __popcll(bal));
+          base = __shfl(base, __ffsll(static_cast<long long>(bal)) - 1, kWave);
+          if (take) {
+            const int pos = base + __popcll(bal & ((1ull << (tid & 63)) - 1ull));
+            if (pos < kcap)
+              cand[pos] = (static_cast<unsigned long long>(k) << 32) |
+                          static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(i));
+          }
+        }
+      }
+    };
+    if (M > kSelScanB * NT) {
+      compact(std::integral_constant<int, kSelScanB>());
+    } else {
+      for (int i = tid; i < M; i += NT) {
+        const uint32_t k = skey[i];
+        if (k == 0u) continue;
+        const bool take = nV <= a.k_max || k > thr ||
+                          (k == thr && (all_eq || 0xFFFFu - static_cast<uint32_t>(i) >= thr_inv));
+        if (take) {
+          const int pos = atomicAdd(&s_count, 1);
+          if (pos < kcap)
+            cand[pos] = (static_cast<unsigned long long>(k) << 32) |
+                        static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(i));
+        }
       }
     }
     __syncthreads();
@@ -1088,7 +1157,7 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int t = 4 * tid + j;
-      e4[j] = t < C ? static_cast<double>(expf(key_to_float(static_cast<uint32_t>(cand[t] >> 32)) - smax))
+      e4[j] = t < C ? static_cast<double>(key_mass(static_cast<uint32_t>(cand[t] >> 32), smax))
                     : 0.0;
       loc += e4[j];
       e4[j] = loc;
@@ -1134,7 +1203,7 @@ __global__ __launch_bounds__(256) void select_gather_kernel(SelectArgs<T> a) {
     mass = pre[K - 1] / Z;
     const double sumI = pre[K - 1];
     for (int t = tid; t < K; t += NT) {
-      const float et = expf(key_to_float(static_cast<uint32_t>(cand[t] >> 32)) - smax);
+      const float et = key_mass(static_cast<uint32_t>(cand[t] >> 32), smax);
       alpha[t] = static_cast<float>(static_cast<double>(et) / sumI);
       const uint32_t ix = 0xFFFFFFFFu - static_cast<uint32_t>(cand[t]);
       sidx[t] = static_cast<int>(min(ix, static_cast<uint32_t>(M - 1)));
