@@ -193,6 +193,26 @@ def test_masked_and_ragged_and_empty(lib, dtype):
         assert case.valid[case.mem_off[b] + sel].all()
 
 
+# No draft nodes at all (every request's node range empty): the call succeeds and
+# launches nothing; a later call on the same context is unaffected.
+def test_no_nodes_at_all(lib):
+    wl = _small("bf16", B=2, T=3)
+    case = make_case(wl)
+    fv = _ctx(lib, wl, case.weights)
+    inp = to_device(case, "bf16")
+    empty = dict(inp, node_off=torch.zeros(wl.B + 1, dtype=torch.int32, device="cuda"),
+                 h=inp["h"][:0].contiguous(), depth=inp["depth"][:0].contiguous())
+    out = fv.retrieve_fuse(empty)
+    torch.cuda.synchronize()
+    st, bits = lib.fovea_last_error(fv.ctx)
+    assert st == 0, bits
+    assert out.h_out.shape[0] == 0
+    g, st, bits = _run(lib, case, fv=fv)
+    assert st == 0, bits
+    compare(case, g, run_oracle(case), H_TOL["bf16"], label="after an empty call")
+    fv.close()
+
+
 @pytest.mark.parametrize("dtype,rows", [("f32", 333), ("bf16", 333), ("bf16", 16400)])
 def test_build_memory(lib, dtype, rows):
     # 333 rows: 128-row tiles; 16400 bf16 rows with d_m = 256: 65 x 4 tiles of 256 rows, the last
